@@ -1,0 +1,187 @@
+/*
+ * ckv.h -- paged KV-cache hot path for multi-turn agent serving on MI355X
+ * (gfx950): append new-turn K/V into a paged pool, prefix-reuse prefill
+ * attention, paged decode attention.
+ *
+ * Why this path exists: Continuum (arXiv 2511.02230) keeps a tool-calling
+ * request's KV blocks resident in GPU memory for a time-to-live instead of
+ * freeing them when the request finishes (Sec. 5.2, "Request Pinning"), so
+ * the program's next turn finds its prefix's pages still in the pool and only
+ * the new tokens (tool output + next prompt) need prefilling (Sec. 1;
+ * Sec. 5.2, "Offline Profile", on pages that stay resident and need no
+ * recomputation).  The paper serves on a paged-attention engine (Sec. 7,
+ * "LLM Inference Systems"); the three calls below are that engine's GPU work
+ * for a retained-prefix turn.  The paper states no attention formula; the one
+ * used is scaled dot-product softmax attention with grouped KV heads.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every pointer argument is a HIP device pointer owned by the caller,
+ *    except the ckv_pool_t / ckv_batch_t structs themselves (host memory,
+ *    read during the call only).  The library keeps no state, never
+ *    allocates or frees memory and never synchronizes; all work is enqueued
+ *    on `stream` (0 = the null stream).  Calls are re-entrant.
+ *  - Pool layout: K and V are each [num_pages][num_kv_heads][page_size]
+ *    [head_dim], row-major, element type kv_dtype.  For CKV_FP8_E4M3 each
+ *    (page, kv head) has an fp32 scale in k_scale / v_scale
+ *    [num_pages][num_kv_heads]; a stored code c represents e4m3(c) * scale.
+ *  - Sequence b's token at absolute position j lives in physical page
+ *    block_table[b * max_pages_per_seq + j / page_size], slot j % page_size.
+ *  - Packed rows: the new-turn rows of sequence b are rows
+ *    cu_q_lens[b] .. cu_q_lens[b+1]-1 of q / k_new / v_new / out, row t of
+ *    sequence b being its token at absolute position ctx_lens[b] + t.
+ *  - Query head h reads KV head h / (num_q_heads / num_kv_heads).
+ *  - Visibility: the query at absolute position i sees key j iff j <= i and,
+ *    when window > 0, i - j < window (exactly `window` keys, itself included).
+ *  - Device-side contents are the caller's contract: page ids must lie in
+ *    [0, num_pages) and every addressed position inside the sequence's
+ *    table; cu_q_lens must be non-decreasing with cu_q_lens[0] = 0 and
+ *    cu_q_lens[num_seqs] = total_q_len; per-sequence lengths must not exceed
+ *    the host-side bounds max_q_len / max_ctx_len.  Violations are undefined
+ *    behaviour (out-of-bounds device accesses); ckv_validate_batch checks
+ *    host copies of these arrays.
+ *  - Host-side argument errors return CKV_ERR_INVALID_ARG, combinations
+ *    without a kernel return CKV_ERR_UNSUPPORTED, a too-small workspace
+ *    returns CKV_ERR_WORKSPACE; nothing is launched in those cases.  A failed
+ *    launch returns CKV_ERR_LAUNCH.
+ *
+ * Supported combinations: (q, pool) dtypes (F32, F32), (BF16, BF16) and
+ * (BF16, FP8_E4M3); head_dim in {64, 128, 256}; page_size in {16, 64};
+ * num_q_heads a multiple of num_kv_heads.
+ */
+#ifndef CKV_H
+#define CKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CKV_OK = 0,
+  CKV_ERR_INVALID_ARG = 1,
+  CKV_ERR_UNSUPPORTED = 2,
+  CKV_ERR_WORKSPACE = 3,
+  CKV_ERR_LAUNCH = 4
+} ckv_status_t;
+
+typedef enum {
+  CKV_F32 = 0,
+  CKV_BF16 = 1,
+  CKV_FP8_E4M3 = 2 /* OCP E4M3FN: bias 7, max 448, no inf, NaN = S.1111.111 */
+} ckv_dtype_t;
+
+/* The paged KV pool: pages retained between turns (Sec. 5.2 pins them). */
+typedef struct {
+  void *k_pages;        /* [num_pages][num_kv_heads][page_size][head_dim] */
+  void *v_pages;        /* same layout */
+  const float *k_scale; /* [num_pages][num_kv_heads], FP8 only, else NULL */
+  const float *v_scale; /* same */
+  int32_t num_pages;
+  int32_t num_kv_heads;
+  int32_t page_size;
+  int32_t head_dim;
+  ckv_dtype_t kv_dtype;
+} ckv_pool_t;
+
+/* One launch's sequences: block tables and context/query lengths. */
+typedef struct {
+  int32_t num_seqs;
+  int32_t max_pages_per_seq;   /* row stride of block_table */
+  const int32_t *block_table;  /* [num_seqs][max_pages_per_seq] physical page ids */
+  const int32_t *ctx_lens;     /* [num_seqs] append / prefill: tokens resident before
+                                  this call (the retained prefix P_b);
+                                  decode: context length c_b >= 1, the query being
+                                  the token at position c_b - 1 */
+  const int32_t *cu_q_lens;    /* [num_seqs + 1] packed row offsets (append / prefill);
+                                  ignored by decode (one row per sequence) */
+  int32_t total_q_len;         /* host copy of cu_q_lens[num_seqs]; decode: num_seqs */
+  int32_t max_q_len;           /* host upper bound of cu_q_lens[b+1] - cu_q_lens[b] */
+  int32_t max_ctx_len;         /* host upper bound of ctx_lens[b] */
+} ckv_batch_t;
+
+/*
+ * kv_append -- write the new turn's keys and values into the pool.
+ * For every sequence b and row t < n_b: position j = ctx_lens[b] + t; for each
+ * KV head h, K[page(j)][h][j % page_size][:] = enc(k_new[cu_q_lens[b] + t][h][:]),
+ * likewise V.  No other pool byte changes.
+ *   k_new, v_new: [total_q_len][num_kv_heads][head_dim], element type in_dtype.
+ *   enc: bit copy when in_dtype == kv_dtype (F32 or BF16); for BF16 -> FP8_E4M3,
+ *        r = x / scale[page][h] in IEEE binary32 (round to nearest even), clamped
+ *        to [-448, 448], rounded to nearest-even E4M3FN (-0 -> 0x80).  NaN inputs
+ *        give a NaN code.  The scales are inputs (the caller's policy).
+ * Rows of different sequences must address distinct slots.
+ */
+ckv_status_t kv_append(const ckv_pool_t *pool, const ckv_batch_t *batch,
+                       const void *k_new, const void *v_new, ckv_dtype_t in_dtype,
+                       hipStream_t stream);
+
+/*
+ * prefix_prefill_attn -- causal attention of the new-turn queries over the
+ * retained prefix plus the new turn itself (call kv_append first).
+ * For row t of sequence b (position i = ctx_lens[b] + t) and query head h:
+ *   out[row][h][:] = sum_{j visible} e^{s_j - m} V_j / sum_{j visible} e^{s_j - m},
+ *   s_j = softmax_scale * <q[row][h][:], K_j>, m = max_j s_j,
+ * K_j, V_j being KV head h / G of position j read through the block table.
+ *   q, out: [total_q_len][num_q_heads][head_dim]; out has q_dtype.
+ *   Softmax and accumulation are fp32; BF16 products run on MFMA in bf16.
+ *   workspace: at least prefix_prefill_workspace_bytes(...) bytes (may be 0).
+ */
+ckv_status_t prefix_prefill_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
+                                 const void *q, ckv_dtype_t q_dtype, int32_t num_q_heads,
+                                 float softmax_scale, int32_t window, void *out,
+                                 void *workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
+/*
+ * paged_decode_attn -- one query per sequence at position c_b - 1 over its
+ * c_b = ctx_lens[b] tokens (its own K/V already appended).  Same formula.
+ *   q, out: [num_seqs][num_q_heads][head_dim]; out has q_dtype.
+ *   kv_split_len: keys per split-K partition (0 = library choice, else a
+ *   positive multiple of 64).  Partitions are fixed by logical positions only,
+ *   so results do not depend on physical page placement.
+ *   workspace: at least paged_decode_workspace_bytes(...) bytes.
+ */
+ckv_status_t paged_decode_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
+                               const void *q, ckv_dtype_t q_dtype, int32_t num_q_heads,
+                               float softmax_scale, int32_t window, int32_t kv_split_len,
+                               void *out, void *workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+
+/* Workspace sizes in bytes for the calls above (0 when none is needed).
+ * Return 0 as well for invalid arguments, which the calls then reject. */
+size_t prefix_prefill_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t *batch,
+                                      int32_t num_q_heads);
+size_t paged_decode_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t *batch,
+                                    int32_t num_q_heads, int32_t kv_split_len);
+
+/*
+ * ckv_validate_batch -- host-side check of the device-side contract, on HOST
+ * copies of block_table (num_seqs * max_pages_per_seq entries), ctx_lens and
+ * cu_q_lens (NULL for decode).  mode 0 = append/prefill (positions up to
+ * ctx_lens[b] + n_b - 1 must be mapped), mode 1 = decode (up to ctx_lens[b] - 1,
+ * ctx_lens[b] >= 1).  Checks page ids in range, lengths within the host bounds
+ * and the table, and distinct pages across sequences when distinct_pages != 0.
+ * Returns CKV_OK or CKV_ERR_INVALID_ARG.  Pure host code; needs no GPU.
+ */
+ckv_status_t ckv_validate_batch(const ckv_pool_t *pool, int32_t num_seqs,
+                                int32_t max_pages_per_seq, const int32_t *block_table_host,
+                                const int32_t *ctx_lens_host, const int32_t *cu_q_lens_host,
+                                int32_t max_q_len, int32_t max_ctx_len, int32_t mode,
+                                int32_t distinct_pages);
+
+/* Human-readable name of a status code (static storage). */
+const char *ckv_status_string(ckv_status_t status);
+
+/* Library version as major * 10000 + minor * 100 + patch. */
+int32_t ckv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CKV_H */

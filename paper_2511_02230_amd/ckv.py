@@ -1,0 +1,261 @@
+"""ctypes binding of libckv.so: argument marshalling only.
+
+Every step of the hot path runs in the library's HIP kernels; this module
+checks tensor dtypes / shapes / devices, fills the C structs of the C ABI
+(include/ckv.h) and passes raw device pointers plus the current HIP stream.
+It never computes anything itself and has no fallback: if libckv.so is
+missing or fails to load, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional
+
+import numpy as np
+import torch  # must be loaded first: libckv.so then binds to torch's HIP runtime
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libckv.so")
+
+CKV_F32, CKV_BF16, CKV_FP8_E4M3 = 0, 1, 2
+STATUS = {0: "CKV_OK", 1: "CKV_ERR_INVALID_ARG", 2: "CKV_ERR_UNSUPPORTED", 3: "CKV_ERR_WORKSPACE",
+          4: "CKV_ERR_LAUNCH"}
+EXPORTS = ("kv_append", "prefix_prefill_attn", "paged_decode_attn", "prefix_prefill_workspace_bytes",
+           "paged_decode_workspace_bytes", "ckv_validate_batch", "ckv_status_string", "ckv_version")
+
+
+class CkvError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn} failed: {STATUS.get(code, code)}")
+        self.code = code
+
+
+class PoolT(ctypes.Structure):
+    _fields_ = [("k_pages", ctypes.c_void_p), ("v_pages", ctypes.c_void_p),
+                ("k_scale", ctypes.c_void_p), ("v_scale", ctypes.c_void_p),
+                ("num_pages", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("kv_dtype", ctypes.c_int)]
+
+
+class BatchT(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+                ("block_table", ctypes.c_void_p), ("ctx_lens", ctypes.c_void_p),
+                ("cu_q_lens", ctypes.c_void_p), ("total_q_len", ctypes.c_int32),
+                ("max_q_len", ctypes.c_int32), ("max_ctx_len", ctypes.c_int32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2511_02230_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, B = ctypes.POINTER(PoolT), ctypes.POINTER(BatchT)
+    vp, i32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+    sig = {
+        "kv_append": ([P, B, vp, vp, ctypes.c_int, vp], ctypes.c_int),
+        "prefix_prefill_attn": ([P, B, vp, ctypes.c_int, i32, f32, i32, vp, vp, sz, vp], ctypes.c_int),
+        "paged_decode_attn": ([P, B, vp, ctypes.c_int, i32, f32, i32, i32, vp, vp, sz, vp], ctypes.c_int),
+        "prefix_prefill_workspace_bytes": ([P, B, i32], sz),
+        "paged_decode_workspace_bytes": ([P, B, i32, i32], sz),
+        "ckv_validate_batch": ([P, i32, i32, vp, vp, vp, i32, i32, i32, i32], ctypes.c_int),
+        "ckv_status_string": ([ctypes.c_int], ctypes.c_char_p),
+        "ckv_version": ([], i32),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+LIB = _load()
+
+_KV_DTYPES = {torch.float32: CKV_F32, torch.bfloat16: CKV_BF16, torch.uint8: CKV_FP8_E4M3}
+_Q_DTYPES = {torch.float32: CKV_F32, torch.bfloat16: CKV_BF16}
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+@dataclasses.dataclass
+class Pool:
+    """Paged KV pool: k/v [num_pages, H_kv, page_size, D] (float32, bfloat16,
+    or uint8 E4M3FN codes with float32 k_scale / v_scale [num_pages, H_kv])."""
+
+    k: torch.Tensor
+    v: torch.Tensor
+    k_scale: Optional[torch.Tensor] = None
+    v_scale: Optional[torch.Tensor] = None
+
+    def __post_init__(self):
+        _dev(self.k, "pool.k")
+        _dev(self.v, "pool.v", self.k.dtype)
+        if self.k.dim() != 4 or self.v.shape != self.k.shape:
+            raise ValueError("pool tensors must be [num_pages, H_kv, page_size, D]")
+        if self.k.dtype not in _KV_DTYPES:
+            raise ValueError(f"unsupported pool dtype {self.k.dtype}")
+        if self.k.dtype == torch.uint8:
+            if self.k_scale is None or self.v_scale is None:
+                raise ValueError("fp8 pool needs k_scale and v_scale")
+            for nm, s in (("k_scale", self.k_scale), ("v_scale", self.v_scale)):
+                _dev(s, nm, torch.float32)
+                if tuple(s.shape) != tuple(self.k.shape[:2]):
+                    raise ValueError(f"{nm} must be [num_pages, H_kv]")
+
+    @property
+    def kv_dtype(self) -> int:
+        return _KV_DTYPES[self.k.dtype]
+
+    def c(self) -> PoolT:
+        n, h, ps, d = self.k.shape
+        return PoolT(_ptr(self.k), _ptr(self.v), _ptr(self.k_scale), _ptr(self.v_scale), n, h, ps, d,
+                     self.kv_dtype)
+
+
+@dataclasses.dataclass
+class Batch:
+    """Block tables and lengths on the GPU (int32) plus host-side bounds."""
+
+    block_table: torch.Tensor  # [B, max_pages] int32
+    ctx_lens: torch.Tensor     # [B] int32
+    cu_q_lens: Optional[torch.Tensor]  # [B+1] int32 (append / prefill)
+    total_q_len: int
+    max_q_len: int
+    max_ctx_len: int
+
+    def __post_init__(self):
+        _dev(self.block_table, "block_table", torch.int32)
+        _dev(self.ctx_lens, "ctx_lens", torch.int32)
+        if self.cu_q_lens is not None:
+            _dev(self.cu_q_lens, "cu_q_lens", torch.int32)
+
+    @property
+    def num_seqs(self) -> int:
+        return int(self.ctx_lens.shape[0])
+
+    def c(self) -> BatchT:
+        return BatchT(self.num_seqs, int(self.block_table.shape[1]), _ptr(self.block_table),
+                      _ptr(self.ctx_lens), _ptr(self.cu_q_lens), int(self.total_q_len),
+                      int(self.max_q_len), int(self.max_ctx_len))
+
+
+def _check(name: str, code: int):
+    if code != 0:
+        raise CkvError(name, code)
+
+
+def kv_append(pool: Pool, batch: Batch, k_new: torch.Tensor, v_new: torch.Tensor, stream=None):
+    """Write new-turn rows k_new / v_new [total_q_len, H_kv, D] into the pool."""
+    _dev(k_new, "k_new")
+    _dev(v_new, "v_new", k_new.dtype)
+    if k_new.dtype not in _Q_DTYPES:
+        raise ValueError(f"unsupported k_new dtype {k_new.dtype}")
+    if tuple(k_new.shape) != (batch.total_q_len,) + tuple(pool.k.shape[1:2]) + tuple(pool.k.shape[3:]):
+        raise ValueError("k_new must be [total_q_len, H_kv, D]")
+    pc, bc = pool.c(), batch.c()
+    _check("kv_append", LIB.kv_append(ctypes.byref(pc), ctypes.byref(bc), _ptr(k_new), _ptr(v_new),
+                                      _Q_DTYPES[k_new.dtype], _stream(stream)))
+
+
+def prefill_workspace_bytes(pool: Pool, batch: Batch, num_q_heads: int) -> int:
+    pc, bc = pool.c(), batch.c()
+    return int(LIB.prefix_prefill_workspace_bytes(ctypes.byref(pc), ctypes.byref(bc), num_q_heads))
+
+
+def decode_workspace_bytes(pool: Pool, batch: Batch, num_q_heads: int, kv_split_len: int = 0) -> int:
+    pc, bc = pool.c(), batch.c()
+    return int(LIB.paged_decode_workspace_bytes(ctypes.byref(pc), ctypes.byref(bc), num_q_heads,
+                                                kv_split_len))
+
+
+def _out_like(q, out):
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, "out", q.dtype)
+    if out.shape != q.shape:
+        raise ValueError("out must have q's shape")
+    return out
+
+
+def _workspace(nbytes: int, workspace, device):
+    if nbytes == 0:
+        return None, 0
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    _dev(workspace, "workspace")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def prefix_prefill_attn(pool: Pool, batch: Batch, q: torch.Tensor, softmax_scale: float,
+                        window: int = 0, out=None, workspace=None, stream=None) -> torch.Tensor:
+    """Causal GQA attention of the new-turn rows q [total_q_len, H_q, D]."""
+    _dev(q, "q")
+    if q.dtype not in _Q_DTYPES or q.dim() != 3 or q.shape[0] != batch.total_q_len:
+        raise ValueError("q must be [total_q_len, H_q, D] float32 or bfloat16")
+    out = _out_like(q, out)
+    ws, wsb = _workspace(prefill_workspace_bytes(pool, batch, q.shape[1]), workspace, q.device)
+    pc, bc = pool.c(), batch.c()
+    _check("prefix_prefill_attn", LIB.prefix_prefill_attn(
+        ctypes.byref(pc), ctypes.byref(bc), _ptr(q), _Q_DTYPES[q.dtype], q.shape[1],
+        float(softmax_scale), int(window), _ptr(out), _ptr(ws), wsb, _stream(stream)))
+    return out
+
+
+def paged_decode_attn(pool: Pool, batch: Batch, q: torch.Tensor, softmax_scale: float,
+                      window: int = 0, kv_split_len: int = 0, out=None, workspace=None,
+                      stream=None) -> torch.Tensor:
+    """Decode attention of q [B, H_q, D]; batch.ctx_lens holds c_b."""
+    _dev(q, "q")
+    if q.dtype not in _Q_DTYPES or q.dim() != 3 or q.shape[0] != batch.num_seqs:
+        raise ValueError("q must be [num_seqs, H_q, D] float32 or bfloat16")
+    out = _out_like(q, out)
+    ws, wsb = _workspace(decode_workspace_bytes(pool, batch, q.shape[1], kv_split_len), workspace,
+                         q.device)
+    pc, bc = pool.c(), batch.c()
+    _check("paged_decode_attn", LIB.paged_decode_attn(
+        ctypes.byref(pc), ctypes.byref(bc), _ptr(q), _Q_DTYPES[q.dtype], q.shape[1],
+        float(softmax_scale), int(window), int(kv_split_len), _ptr(out), _ptr(ws), wsb,
+        _stream(stream)))
+    return out
+
+
+def validate_batch(num_pages: int, page_size: int, block_table: np.ndarray, ctx_lens: np.ndarray,
+                   cu_q_lens: Optional[np.ndarray], max_q_len: int, max_ctx_len: int, decode: bool,
+                   distinct_pages: bool = False) -> None:
+    """Host-side check (C ABI ckv_validate_batch) of block tables and lengths
+    before a launch; raises CkvError on a violation."""
+    bt = np.ascontiguousarray(block_table, dtype=np.int32)
+    ctx = np.ascontiguousarray(ctx_lens, dtype=np.int32)
+    cu = None if cu_q_lens is None else np.ascontiguousarray(cu_q_lens, dtype=np.int32)
+    pc = PoolT(None, None, None, None, num_pages, 1, page_size, 64, CKV_BF16)
+    code = LIB.ckv_validate_batch(ctypes.byref(pc), len(ctx), bt.shape[1] if bt.ndim == 2 else 0,
+                                  bt.ctypes.data, ctx.ctypes.data,
+                                  None if cu is None else cu.ctypes.data, max_q_len, max_ctx_len,
+                                  1 if decode else 0, 1 if distinct_pages else 0)
+    _check("ckv_validate_batch", code)
+
+
+def status_string(code: int) -> str:
+    return LIB.ckv_status_string(code).decode()
+
+
+def version() -> int:
+    return int(LIB.ckv_version())

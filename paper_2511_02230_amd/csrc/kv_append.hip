@@ -1,0 +1,120 @@
+// kv_append: scatter the new turn's K/V rows into their pool slots through
+// the block table (bit copy, or bf16 -> fp8 E4M3FN with a per-(page, head)
+// scale).  HBM-bound: each 16-byte input chunk is read once and written once.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace ckv {
+namespace {
+
+struct AppendArgs {
+  const uint8_t *k_new, *v_new;
+  uint8_t *k_pool, *v_pool;
+  const float *k_scale, *v_scale;
+  const int32_t *bt, *ctx, *cu;
+  int32_t max_pages, h, ps;
+  int32_t units;       // 16-byte input chunks per (token, head) row
+  int32_t in_row, out_row;  // bytes per (token, head) row in the input / pool
+  int32_t tok_per_block;
+};
+
+// Quantize 8 bf16 values (one 16-byte chunk) to 8 E4M3FN codes:
+// r = x / s (IEEE binary32 division), clamp to +-448, round to nearest even.
+__device__ __forceinline__ u32x2 quantize8(u32x4 x, float s) {
+  float f[8];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    f[2 * w] = bf16_lo(x[w]);
+    f[2 * w + 1] = bf16_hi(x[w]);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    float r = f[i] / s;
+    float c = fminf(fmaxf(r, -448.0f), 448.0f);
+    f[i] = (r != r) ? r : c;
+  }
+  u32x2 out;
+  int w0 = __builtin_amdgcn_cvt_pk_fp8_f32(f[0], f[1], 0, false);
+  w0 = __builtin_amdgcn_cvt_pk_fp8_f32(f[2], f[3], w0, true);
+  int w1 = __builtin_amdgcn_cvt_pk_fp8_f32(f[4], f[5], 0, false);
+  w1 = __builtin_amdgcn_cvt_pk_fp8_f32(f[6], f[7], w1, true);
+  out.x = (uint32_t)w0;
+  out.y = (uint32_t)w1;
+  return out;
+}
+
+// Grid: x = token chunks of one sequence, y = sequence.  Each thread moves
+// 16-byte chunks; consecutive threads cover consecutive chunks of a row, and
+// a (token, head) row is contiguous both in the packed input and in its page.
+template <bool FP8>
+__global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
+  const int b = blockIdx.y;
+  const int q0 = a.cu[b];
+  const int n = a.cu[b + 1] - q0;
+  const int t0 = blockIdx.x * a.tok_per_block;
+  if (t0 >= n) return;
+  const int P = a.ctx[b];
+  const int tcount = min(a.tok_per_block, n - t0);
+  const int per_head = a.units;
+  const int per_kv = a.h * per_head;
+  const int per_tok = 2 * per_kv;
+  const int total = tcount * per_tok;
+  const int32_t *bt = a.bt + (size_t)b * a.max_pages;
+  for (int u = threadIdx.x; u < total; u += blockDim.x) {
+    const int tt = u / per_tok;
+    int r = u - tt * per_tok;
+    const int kv = r / per_kv;
+    r -= kv * per_kv;
+    const int hh = r / per_head;
+    const int c = r - hh * per_head;
+    const int t = t0 + tt;
+    const int pos = P + t;
+    const int page = bt[pos / a.ps];
+    const int slot = pos - (pos / a.ps) * a.ps;
+    const uint8_t *src = (kv ? a.v_new : a.k_new) + ((size_t)(q0 + t) * a.h + hh) * a.in_row + c * 16;
+    uint8_t *dst = (kv ? a.v_pool : a.k_pool) + (((size_t)page * a.h + hh) * a.ps + slot) * a.out_row;
+    const u32x4 x = ld<u32x4>(src);
+    if constexpr (!FP8) {
+      st<u32x4>(dst + c * 16, x);
+    } else {
+      const float s = (kv ? a.v_scale : a.k_scale)[(size_t)page * a.h + hh];
+      st<u32x2>(dst + c * 8, quantize8(x, s));
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_kv_append(const PoolView &p, const BatchView &b, const void *k_new,
+                            const void *v_new, int in_dtype, hipStream_t s) {
+  if (b.num_seqs == 0 || b.max_q == 0 || b.total_q == 0) return hipSuccess;
+  const int e_in = in_dtype == 0 ? 4 : 2;
+  const bool fp8 = p.kv_dtype == 2;
+  const int e_out = p.kv_dtype == 0 ? 4 : (p.kv_dtype == 1 ? 2 : 1);
+  AppendArgs a;
+  a.k_new = static_cast<const uint8_t *>(k_new);
+  a.v_new = static_cast<const uint8_t *>(v_new);
+  a.k_pool = static_cast<uint8_t *>(p.k);
+  a.v_pool = static_cast<uint8_t *>(p.v);
+  a.k_scale = p.k_scale;
+  a.v_scale = p.v_scale;
+  a.bt = b.bt;
+  a.ctx = b.ctx;
+  a.cu = b.cu_q;
+  a.max_pages = b.max_pages;
+  a.h = p.h_kv;
+  a.ps = p.ps;
+  a.in_row = p.d * e_in;
+  a.out_row = p.d * e_out;
+  a.units = a.in_row / 16;
+  const int per_tok = 2 * p.h_kv * a.units;
+  a.tok_per_block = per_tok >= 1024 ? 1 : 1024 / per_tok;
+  dim3 grid((b.max_q + a.tok_per_block - 1) / a.tok_per_block, b.num_seqs);
+  if (fp8)
+    hipLaunchKernelGGL(kv_append_kernel<true>, grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(kv_append_kernel<false>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace ckv

@@ -1,0 +1,38 @@
+// Internal launcher interface between the C ABI (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ckv {
+
+struct PoolView {
+  void *k, *v;
+  const float *k_scale, *v_scale;
+  int32_t num_pages, h_kv, ps, d;
+  int kv_dtype;  // ckv_dtype_t
+};
+
+struct BatchView {
+  int32_t num_seqs, max_pages;
+  const int32_t *bt, *ctx, *cu_q;
+  int32_t total_q, max_q, max_ctx;
+};
+
+hipError_t launch_kv_append(const PoolView &p, const BatchView &b, const void *k_new,
+                            const void *v_new, int in_dtype, hipStream_t s);
+
+hipError_t launch_attn_f32(const PoolView &p, const BatchView &b, const float *q, int h_q,
+                           float scale, int window, bool decode, float *out, hipStream_t s);
+
+hipError_t launch_prefill_bf16(const PoolView &p, const BatchView &b, const void *q, int h_q,
+                               float scale, int window, void *out, hipStream_t s);
+
+size_t decode_workspace_bytes(const PoolView &p, const BatchView &b, int h_q, int split_len);
+int decode_split_len(const PoolView &p, const BatchView &b, int h_q, int requested);
+hipError_t launch_decode_bf16(const PoolView &p, const BatchView &b, const void *q, int h_q,
+                              float scale, int window, int split_len, void *out, void *ws,
+                              size_t ws_bytes, hipStream_t s);
+
+}  // namespace ckv

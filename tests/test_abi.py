@@ -1,0 +1,134 @@
+"""The C-ABI library loads, exports every symbol include/ckv.h declares, and
+rejects invalid host-side arguments before launching anything (CPU only:
+no call here reaches a kernel)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ckv.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def ckv():
+    from paper_2511_02230_amd import ckv as mod
+
+    return mod
+
+
+def test_header_declares_the_three_calls():
+    names = declared_functions()
+    for fn in ("kv_append", "prefix_prefill_attn", "paged_decode_attn"):
+        assert fn in names
+
+
+def test_library_exports_every_declared_symbol(ckv):
+    out = subprocess.run(["nm", "-D", "--defined-only", ckv.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if " T " in line)
+    for fn in declared_functions():
+        assert fn in exported, fn
+        assert getattr(ckv.LIB, fn) is not None
+    assert set(ckv.EXPORTS) == set(declared_functions())
+
+
+def test_status_strings_and_version(ckv):
+    for code in range(5):
+        assert ckv.status_string(code).startswith(ckv.STATUS[code])
+    assert ckv.version() >= 100
+
+
+def _pool(ckv, **kw):
+    base = dict(k_pages=1, v_pages=1, k_scale=None, v_scale=None, num_pages=4, num_kv_heads=2,
+                page_size=16, head_dim=128, kv_dtype=ckv.CKV_BF16)
+    base.update(kw)
+    return ckv.PoolT(**base)
+
+
+def _batch(ckv, **kw):
+    base = dict(num_seqs=1, max_pages_per_seq=2, block_table=1, ctx_lens=1, cu_q_lens=1,
+                total_q_len=4, max_q_len=4, max_ctx_len=8)
+    base.update(kw)
+    return ckv.BatchT(**base)
+
+
+def _append(ckv, pool, batch, k=1, v=1, in_dtype=1):
+    return ckv.LIB.kv_append(ctypes.byref(pool) if pool is not None else None,
+                             ctypes.byref(batch) if batch is not None else None, k, v, in_dtype, None)
+
+
+def test_append_argument_checks(ckv):
+    assert _append(ckv, None, _batch(ckv)) == 1
+    assert _append(ckv, _pool(ckv, k_pages=None), _batch(ckv)) == 1
+    assert _append(ckv, _pool(ckv, num_pages=0), _batch(ckv)) == 1
+    assert _append(ckv, _pool(ckv, head_dim=96), _batch(ckv)) == 2
+    assert _append(ckv, _pool(ckv, page_size=32), _batch(ckv)) == 2
+    assert _append(ckv, _pool(ckv, kv_dtype=ckv.CKV_FP8_E4M3), _batch(ckv)) == 1  # no scales
+    assert _append(ckv, _pool(ckv), _batch(ckv), in_dtype=0) == 2  # f32 into a bf16 pool
+    assert _append(ckv, _pool(ckv), _batch(ckv, cu_q_lens=None)) == 1
+    assert _append(ckv, _pool(ckv), _batch(ckv, max_ctx_len=40)) == 1  # beyond the table
+    assert _append(ckv, _pool(ckv), _batch(ckv), k=None) == 1
+    assert _append(ckv, _pool(ckv), _batch(ckv, num_seqs=0)) == 0  # nothing to do
+    assert _append(ckv, _pool(ckv), _batch(ckv, total_q_len=0)) == 0
+
+
+def test_attention_argument_checks(ckv):
+    P, B = _pool(ckv), _batch(ckv)
+    f = ckv.LIB.prefix_prefill_attn
+    assert f(ctypes.byref(P), ctypes.byref(B), 1, 1, 3, 0.1, 0, 1, None, 0, None) == 1  # 3 % 2
+    assert f(ctypes.byref(P), ctypes.byref(B), 1, 0, 4, 0.1, 0, 1, None, 0, None) == 2  # f32 q, bf16 pool
+    assert f(ctypes.byref(P), ctypes.byref(B), 1, 1, 4, float("nan"), 0, 1, None, 0, None) == 1
+    assert f(ctypes.byref(P), ctypes.byref(B), 1, 1, 4, 0.1, -1, 1, None, 0, None) == 1
+    assert f(ctypes.byref(P), ctypes.byref(B), None, 1, 4, 0.1, 0, 1, None, 0, None) == 1
+    d = ckv.LIB.paged_decode_attn
+    DB = _batch(ckv, cu_q_lens=None, max_ctx_len=20000, max_pages_per_seq=2000)
+    assert d(ctypes.byref(P), ctypes.byref(DB), 1, 1, 4, 0.1, 0, 100, 1, None, 0, None) == 1  # split % 64
+    need = ckv.LIB.paged_decode_workspace_bytes(ctypes.byref(P), ctypes.byref(DB), 4, 0)
+    assert need > 0
+    assert d(ctypes.byref(P), ctypes.byref(DB), 1, 1, 4, 0.1, 0, 0, 1, None, 0, None) == 3
+    assert d(ctypes.byref(P), ctypes.byref(DB), 1, 1, 4, 0.1, 0, 0, 1, 1, need - 1, None) == 3
+    assert d(ctypes.byref(P), ctypes.byref(_batch(ckv, max_ctx_len=0)), 1, 1, 4, 0.1, 0, 0, 1, None,
+             0, None) == 1
+
+
+def test_decode_workspace_grows_with_splits(ckv):
+    P = _pool(ckv)
+    DB = _batch(ckv, cu_q_lens=None, max_ctx_len=4096, max_pages_per_seq=256)
+    a = ckv.LIB.paged_decode_workspace_bytes(ctypes.byref(P), ctypes.byref(DB), 4, 512)
+    b = ckv.LIB.paged_decode_workspace_bytes(ctypes.byref(P), ctypes.byref(DB), 4, 1024)
+    assert a == 1 * 4 * 8 * (128 + 2) * 4 and b == 1 * 4 * 4 * (128 + 2) * 4
+    assert ckv.LIB.paged_decode_workspace_bytes(ctypes.byref(P), ctypes.byref(DB), 4, 4096) == 0
+
+
+def test_validate_batch(ckv):
+    bt = np.array([[3, 1, 0], [2, 0, 0]], np.int32)
+    ckv.validate_batch(4, 16, bt, [20, 5], [0, 10, 12], 10, 20, decode=False)
+    ckv.validate_batch(4, 16, bt, [40, 16], None, 1, 40, decode=True, distinct_pages=False)
+    with pytest.raises(ckv.CkvError):  # page id out of range
+        ckv.validate_batch(3, 16, bt, [20, 5], [0, 10, 12], 10, 20, decode=False)
+    with pytest.raises(ckv.CkvError):  # positions beyond the table
+        ckv.validate_batch(4, 16, bt, [40, 5], [0, 10, 12], 10, 40, decode=False)
+    with pytest.raises(ckv.CkvError):  # shared page across sequences
+        ckv.validate_batch(4, 16, np.array([[3, 1], [1, 0]], np.int32), [20, 5], [0, 1, 2], 1, 20,
+                           decode=False, distinct_pages=True)
+    with pytest.raises(ckv.CkvError):  # decode context 0
+        ckv.validate_batch(4, 16, bt, [0, 5], None, 1, 40, decode=True)
+    with pytest.raises(ckv.CkvError):  # bound violated
+        ckv.validate_batch(4, 16, bt, [20, 5], [0, 10, 12], 9, 20, decode=False)
+
+
+def test_binding_rejects_cpu_tensors(ckv):
+    import torch
+
+    with pytest.raises(ValueError):
+        ckv.Pool(torch.zeros(2, 1, 16, 64), torch.zeros(2, 1, 16, 64))

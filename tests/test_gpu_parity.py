@@ -1,0 +1,276 @@
+"""GPU parity of libckv against the fp64 oracle (needs an MI355X).
+
+Every case runs the HIP kernels through the C ABI (via the ctypes binding)
+on seeded synthetic inputs and compares with the oracle on the same inputs:
+  kv_append            bit-exact, pool page by page (poisoned slots must
+                       stay poisoned)
+  attention, f32       max |err| <= 1e-5
+  attention, bf16      max |err| <= 2e-2 and mean |err| <= 2e-3
+  attention, fp8 KV    max |err| <= 3e-2
+Small cases compare every output; the full-size configurations (in the
+launch configuration the benchmark times) compare sampled sequences / rows.
+"""
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import workload
+from oracle import formats
+from tests.oracle_inputs import OracleState, to_numpy
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": (1e-5, None), "bf16": (2e-2, 2e-3), "fp8": (3e-2, 2e-3)}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2511_02230_amd import ckv  # noqa: F401  (fails loudly if libckv.so is missing)
+
+
+def tol_of(cfg):
+    return TOL["fp8" if cfg.kv_dtype == "fp8" else cfg.q_dtype]
+
+
+def out_f64(t):
+    x = to_numpy(t)
+    return formats.bf16_bits_to_f64(x) if x.dtype == np.uint16 else x.astype(np.float64)
+
+
+def check_close(got, ref, cfg, what):
+    mx_tol, mean_tol = tol_of(cfg)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    err = np.abs(got - ref)
+    mx, mean = float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
+    say(f"  {what}: max {mx:.3e} mean {mean:.3e}")
+    assert mx <= mx_tol, f"{what}: max abs err {mx} > {mx_tol}"
+    if mean_tol is not None:
+        assert mean <= mean_tol, f"{what}: mean abs err {mean} > {mean_tol}"
+
+
+def check_pool(dw, st, what):
+    """GPU pool pages of the oracle's sequences equal the oracle's bytes."""
+    pages = torch.as_tensor(st.pages, device="cuda")
+    for name, gpu, ref in (("K", dw.pool.k, st.pool_k), ("V", dw.pool.v, st.pool_v)):
+        g = to_numpy(gpu.index_select(0, pages))
+        assert g.view(np.uint8).tobytes() == ref.view(np.uint8).tobytes(), f"{what}: {name} pool differs"
+
+
+def check_unused_pages_poisoned(dw, used):
+    mask = torch.ones(dw.wl.num_pages, dtype=torch.bool, device="cuda")
+    mask[torch.as_tensor(np.asarray(used, np.int64), device="cuda")] = False
+    for t in (dw.pool.k, dw.pool.v):
+        rest = t[mask]
+        if t.dtype == torch.uint8:
+            assert bool((rest == 0x7F).all())
+        else:
+            assert bool(torch.isnan(rest.float()).all())
+
+
+def run_case(wl, window=0, prefill_rows=None, decode_rows=None, row_subsets=None, split_lens=(0,)):
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    cfg = wl.cfg
+    pf, dc = wl.prefill, wl.decode
+    pf_rows = list(range(pf.num_seqs)) if prefill_rows is None else list(prefill_rows)
+    dc_rows = list(range(dc.num_seqs)) if decode_rows is None else list(decode_rows)
+    sids = sorted(set(int(pf.seq_ids[b]) for b in pf_rows) | set(int(dc.seq_ids[b]) for b in dc_rows))
+    say(f"case {cfg.name} D={cfg.head_dim} ps={cfg.page_size} G={cfg.group} kv={cfg.kv_dtype} "
+        f"W={window} prefill={pf.num_seqs} decode={dc.num_seqs}")
+    dw = DeviceWorkload(wl, "cuda", window=window)
+    st = OracleState(wl, sids=sids, device="cuda")
+    check_pool(dw, st, "set-up append")
+    if pf.num_seqs:
+        dw.append_prefill()
+        torch.cuda.synchronize()
+        st.append_prefill(pf_rows)
+        check_pool(dw, st, "new-turn append")
+        out = dw.run_prefill()
+        torch.cuda.synchronize()
+        got = out_f64(out)
+        ref = st.prefill(to_numpy(dw.q_prefill), [b for b in pf_rows if b in st.rows_of(pf)], window,
+                         row_subsets)
+        cu = pf.cu_q_lens
+        for b, r in ref.items():
+            t = np.arange(int(pf.q_lens[b])) if row_subsets is None else np.asarray(row_subsets[b])
+            check_close(got[cu[b] + t], r, cfg, f"prefill seq {b} (P={pf.ctx_lens[b]}, n={pf.q_lens[b]})")
+    if dc.num_seqs:
+        dw.append_decode()
+        torch.cuda.synchronize()
+        st.append_decode(dc_rows)
+        check_pool(dw, st, "decode-token append")
+        ref = st.decode(to_numpy(dw.q_decode), st.rows_of(dc, dc_rows), window)
+        for split in split_lens:
+            out = dw.run_decode(kv_split_len=split)
+            torch.cuda.synchronize()
+            got = out_f64(out)
+            for b, r in ref.items():
+                check_close(got[b], r, cfg, f"decode seq {b} (c={wl.decode_ctx[b]}, split={split})")
+    return dw, st
+
+
+# --------------------------------------------------------------- Tiny
+
+def test_tiny_config_whole_pool():
+    wl = workload.make_workload(workload.TINY)
+    dw, st = run_case(wl)
+    check_unused_pages_poisoned(dw, st.pages)
+
+
+# ------------------------------------------------------- small shapes
+
+def cfg_of(name, hq, hkv, d, ps, kv, q="bf16", seed=11):
+    return workload.Config(name, seed, hq, hkv, d, ps, q, kv)
+
+
+SMALL = [
+    # (config, prefill [(P, n)], decode [c], window)
+    (cfg_of("c1", 8, 1, 128, 16, "bf16"), [(0, 1), (5, 40), (130, 67), (0, 300)], [1, 17, 64, 65, 700], 0),
+    (cfg_of("c2", 32, 8, 128, 16, "bf16"), [(100, 33), (1, 1), (257, 130)], [300, 2, 1000], 0),
+    (cfg_of("c3", 16, 8, 256, 16, "bf16"), [(64, 64), (3, 90)], [129, 513], 0),
+    (cfg_of("c4", 4, 4, 64, 64, "bf16"), [(200, 100), (0, 64)], [63, 64, 65], 0),
+    (cfg_of("c5", 96, 8, 128, 64, "fp8"), [(300, 20), (64, 70), (0, 5)], [1, 200, 700], 0),
+    (cfg_of("c6", 12, 1, 128, 16, "fp8"), [(40, 50)], [33, 99], 0),
+    (cfg_of("c7", 20, 1, 64, 16, "bf16"), [(10, 13)], [77], 0),
+    (cfg_of("w1", 16, 8, 256, 16, "bf16"), [(100, 60), (0, 200), (1500, 40)], [300, 1200, 5], 17),
+    (cfg_of("w2", 8, 2, 128, 16, "bf16"), [(50, 50)], [90, 3], 1),
+    (cfg_of("w3", 8, 2, 128, 64, "fp8"), [(500, 100)], [400], 100),
+    (cfg_of("f1", 4, 2, 64, 16, "f32", "f32"), [(30, 20), (0, 3)], [19, 50], 0),
+    (cfg_of("f2", 4, 1, 128, 64, "f32", "f32"), [(70, 9)], [129], 5),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: c[0].name)
+def test_small_shapes(case):
+    cfg, pf, dc, w = case
+    wl = workload.make_workload(cfg, prefill=pf, decode=dc)
+    dw, st = run_case(wl, window=w, split_lens=(0, 64, 128) if cfg.q_dtype == "bf16" else (0,))
+    check_unused_pages_poisoned(dw, st.pages)
+
+
+# ----------------------------------------------------------- full size
+
+def _sample_rows(wl, rng, k_pf=3, k_dc=4):
+    pf, dc = wl.prefill, wl.decode
+    lens = pf.ctx_lens + pf.q_lens
+    pf_rows = sorted(set([int(np.argmax(lens)), int(np.argmin(pf.q_lens))] +
+                         [int(x) for x in rng.choice(pf.num_seqs, k_pf, replace=False)]))[:k_pf + 1]
+    dctx = wl.decode_ctx
+    dc_rows = sorted(set([int(np.argmax(dctx)), int(np.argmin(dctx))] +
+                         [int(x) for x in rng.choice(dc.num_seqs, k_dc, replace=False)]))
+    subsets = {}
+    for b in pf_rows:
+        n = int(pf.q_lens[b])
+        P = int(pf.ctx_lens[b])
+        ps = wl.cfg.page_size
+        edge = [t for t in range(n) if (P + t) % ps in (0, ps - 1)][:8]
+        t = sorted(set([0, n - 1] + edge + [int(x) for x in rng.choice(n, min(n, 12), replace=False)]))
+        subsets[b] = np.array(t)
+    return pf_rows, dc_rows, subsets
+
+
+@pytest.mark.parametrize("name,window", [("llama3.1-8b", 0), ("gemma3-12b", 0), ("gemma3-12b", 1024),
+                                         ("llama3.1-70b", 0), ("glm4.5-355b", 0)])
+def test_full_config_sampled(name, window):
+    cfg = workload.CONFIGS[name]
+    wl = workload.make_workload(cfg)
+    rng = np.random.default_rng([cfg.seed, window, 7])
+    pf_rows, dc_rows, subsets = _sample_rows(wl, rng)
+    run_case(wl, window, pf_rows, dc_rows, subsets)
+
+
+# ----------------------------------------------------------- invariants
+
+def _outputs(wl, window=0):
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    dw = DeviceWorkload(wl, "cuda", window=window)
+    dw.step()
+    torch.cuda.synchronize()
+    return dw.out_prefill.clone(), dw.out_decode.clone()
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+def test_page_shuffle_is_bit_identical(kv):
+    cfg = cfg_of("shuf", 16, 2, 128, 16, kv)
+    pf, dc = [(300, 100), (17, 250)], [1000, 33]
+    a = _outputs(workload.make_workload(cfg, prefill=pf, decode=dc))
+    b = _outputs(workload.make_workload(cfg, prefill=pf, decode=dc, slack_pages=37))
+    for x, y in zip(a, b):
+        assert torch.equal(x.view(torch.int16), y.view(torch.int16))
+
+
+def test_decode_matches_one_row_prefill_on_gpu():
+    from paper_2511_02230_amd import ckv
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    cfg = cfg_of("dvp", 32, 8, 128, 16, "bf16")
+    wl = workload.make_workload(cfg, prefill=[], decode=[1000, 77, 4096])
+    dw = DeviceWorkload(wl, "cuda")
+    dw.append_decode()
+    dec = out_f64(dw.run_decode())
+    dcx = wl.decode_ctx
+    # the same queries as one-row prefills at P = c - 1
+    bt = dw.decode.block_table
+    ctx = torch.as_tensor((dcx - 1).astype(np.int32), device="cuda")
+    cu = torch.arange(len(dcx) + 1, dtype=torch.int32, device="cuda")
+    batch = ckv.Batch(bt, ctx, cu, len(dcx), 1, int(dcx.max()) - 1)
+    pre = out_f64(ckv.prefix_prefill_attn(dw.pool, batch, dw.q_decode, cfg.softmax_scale))
+    assert np.max(np.abs(dec - pre)) <= 2e-2
+
+
+def test_fp8_quantizer_every_bf16_value():
+    """kv_append's bf16 -> E4M3FN encoder on every finite bf16 bit pattern
+    and three scales, against the oracle's encoder."""
+    from paper_2511_02230_amd import ckv
+
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    vals = formats.bf16_bits_to_f64(bits)
+    bits = bits[~np.isnan(vals)]
+    n_tok = -(-len(bits) // 128)
+    pad = n_tok * 128 - len(bits)
+    bits = np.concatenate([bits, np.zeros(pad, np.uint16)])
+    x = torch.from_numpy(bits.view(np.int16).reshape(n_tok, 1, 128)).view(torch.bfloat16).cuda()
+    for scale in (1.0, 0.37, 3.1e-3):
+        npages = -(-n_tok // 64)
+        k = torch.full((npages, 1, 64, 128), 0x7F, dtype=torch.uint8, device="cuda")
+        v = torch.full_like(k, 0x7F)
+        ks = torch.full((npages, 1), scale, dtype=torch.float32, device="cuda")
+        pool = ckv.Pool(k, v, ks, ks.clone())
+        bt = torch.arange(npages, dtype=torch.int32, device="cuda")[None]
+        batch = ckv.Batch(bt, torch.zeros(1, dtype=torch.int32, device="cuda"),
+                          torch.tensor([0, n_tok], dtype=torch.int32, device="cuda"), n_tok, n_tok, 0)
+        ckv.kv_append(pool, batch, x, x)
+        torch.cuda.synchronize()
+        got = k.reshape(-1)[:n_tok * 128].cpu().numpy()
+        ref = formats.fp8_quantize(formats.bf16_bits_to_f32(bits), np.float32(scale))
+        bad = np.nonzero(got != ref)[0]
+        assert bad.size == 0, (scale, bad[:5], bits[bad[:5]], got[bad[:5]], ref[bad[:5]])
+
+
+def test_empty_and_degenerate_batches():
+    from paper_2511_02230_amd import ckv
+
+    cfg = cfg_of("deg", 8, 2, 128, 16, "bf16")
+    wl = workload.make_workload(cfg, prefill=[(20, 0), (0, 1), (16, 16)], decode=[1])
+    run_case(wl)
+    # an empty launch is a no-op
+    dw_pool = ckv.Pool(torch.zeros(1, 2, 16, 128, dtype=torch.bfloat16, device="cuda"),
+                       torch.zeros(1, 2, 16, 128, dtype=torch.bfloat16, device="cuda"))
+    empty = ckv.Batch(torch.zeros((0, 1), dtype=torch.int32, device="cuda"),
+                      torch.zeros(0, dtype=torch.int32, device="cuda"),
+                      torch.zeros(1, dtype=torch.int32, device="cuda"), 0, 0, 0)
+    q = torch.zeros((0, 8, 128), dtype=torch.bfloat16, device="cuda")
+    ckv.kv_append(dw_pool, empty, torch.zeros((0, 2, 128), dtype=torch.bfloat16, device="cuda"),
+                  torch.zeros((0, 2, 128), dtype=torch.bfloat16, device="cuda"))
+    ckv.prefix_prefill_attn(dw_pool, empty, q, 0.1)
+    torch.cuda.synchronize()

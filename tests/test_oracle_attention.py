@@ -106,12 +106,13 @@ def test_oracle_matches_brute_force_tiny_config():
     st.append_prefill()
     q = to_numpy(workload.concat_rows(wl.prefill, lambda b: workload.prefill_q(wl, b)))
     pf = wl.prefill
-    out = paged.prefix_prefill(q, st.pool_k, st.pool_v, pf.block_table, pf.ctx_lens, pf.q_lens,
+    bt = st.table(pf, [0])
+    out = paged.prefix_prefill(q, st.pool_k, st.pool_v, bt, pf.ctx_lens, pf.q_lens,
                                page_size=16, kv_dtype="f32", softmax_scale=0.125)
     rows = [0, 7, 15]
     sel_q = q_to_f64(q, "f32")[rows]
     ref = brute.prefill(sel_q.tolist(), st.pool_k.astype(np.float64).tolist(),
-                        st.pool_v.astype(np.float64).tolist(), [pf.block_table[0].tolist()] * 3,
+                        st.pool_v.astype(np.float64).tolist(), [bt[0].tolist()] * 3,
                         [240 + r for r in rows], [1, 1, 1], 16, 0.125)
     assert np.max(np.abs(out[rows] - np.array(ref))) <= 1e-12
 
