@@ -38,7 +38,7 @@ ckv_status_t check_batch(const ckv_pool_t *p, const ckv_batch_t *b, int mode) {
   if (mode == 0) {
     if (!b->cu_q_lens) return CKV_ERR_INVALID_ARG;
     if (b->total_q_len > (long long)b->num_seqs * b->max_q_len) return CKV_ERR_INVALID_ARG;
-    if ((long long)b->max_ctx_len + b->max_q_len > cap) return CKV_ERR_INVALID_ARG;
+    if (b->max_ctx_len > cap || b->max_q_len > cap) return CKV_ERR_INVALID_ARG;
   } else {
     if (b->max_ctx_len < 1 || b->max_ctx_len > cap) return CKV_ERR_INVALID_ARG;
   }

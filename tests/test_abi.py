@@ -77,6 +77,7 @@ def test_append_argument_checks(ckv):
     assert _append(ckv, _pool(ckv), _batch(ckv), in_dtype=0) == 2  # f32 into a bf16 pool
     assert _append(ckv, _pool(ckv), _batch(ckv, cu_q_lens=None)) == 1
     assert _append(ckv, _pool(ckv), _batch(ckv, max_ctx_len=40)) == 1  # beyond the table
+    assert _append(ckv, _pool(ckv), _batch(ckv, max_q_len=33, total_q_len=4)) == 1
     assert _append(ckv, _pool(ckv), _batch(ckv), k=None) == 1
     assert _append(ckv, _pool(ckv), _batch(ckv, num_seqs=0)) == 0  # nothing to do
     assert _append(ckv, _pool(ckv), _batch(ckv, total_q_len=0)) == 0
