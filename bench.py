@@ -85,12 +85,13 @@ def cpu_baseline(wl, window, budget_s=20.0):
     st = OracleState(wl, sids=[int(pf.seq_ids[b])], device="cuda")
     st.append_prefill([b])
     q = to_numpy(workload.concat_rows(pf, lambda r: workload.prefill_q(wl, r, "cuda")))
-    # grow the sample until it takes a meaningful share of the budget
-    rows = 1
+    # size the sample from a 16-row probe so that it takes about budget_s
+    probe = np.linspace(0, n - 1, min(n, 16)).astype(np.int64)
+    st.prefill(q, [b], window, {b: probe[:2]})  # warm caches / BLAS threads
     t0 = time.perf_counter()
-    st.prefill(q, [b], window, {b: np.array([n - 1])})
-    one = time.perf_counter() - t0
-    rows = int(max(1, min(n, budget_s / max(one, 1e-3))))
+    st.prefill(q, [b], window, {b: probe})
+    per_row = (time.perf_counter() - t0) / len(probe)
+    rows = int(max(1, min(n, budget_s / max(per_row, 1e-4))))
     sel = np.linspace(0, n - 1, rows).astype(np.int64)
     t0 = time.perf_counter()
     st.prefill(q, [b], window, {b: sel})
@@ -113,6 +114,8 @@ def main():
     ap.add_argument("--config", default="llama3.1-70b")
     ap.add_argument("--window", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after timing, run one 512 MiB device-to-device copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the kernels run on one device's share of the work "
@@ -175,6 +178,13 @@ def main():
                       "work": abytes},
         "kv_append_decode": {"bound": "hbm", "ms": per["kv_append_decode"], "work": adbytes},
     }
+    if args.calibrate_copy:
+        src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)

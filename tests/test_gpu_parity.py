@@ -144,6 +144,9 @@ SMALL = [
     (cfg_of("w1", 16, 8, 256, 16, "bf16"), [(100, 60), (0, 200), (1500, 40)], [300, 1200, 5], 17),
     (cfg_of("w2", 8, 2, 128, 16, "bf16"), [(50, 50)], [90, 3], 1),
     (cfg_of("w3", 8, 2, 128, 64, "fp8"), [(500, 100)], [400], 100),
+    # rows whose window starts within the first keys of a block, while other
+    # rows of the same wave already see keys in earlier blocks
+    (cfg_of("w4", 16, 8, 128, 16, "bf16"), [(100, 60), (97, 70)], [130], 40),
     (cfg_of("f1", 4, 2, 64, 16, "f32", "f32"), [(30, 20), (0, 3)], [19, 50], 0),
     (cfg_of("f2", 4, 1, 128, 64, "f32", "f32"), [(70, 9)], [129], 5),
 ]
