@@ -142,8 +142,9 @@ ckv_status_t prefix_prefill_attn(const ckv_pool_t *pool, const ckv_batch_t *batc
  * c_b = ctx_lens[b] tokens (its own K/V already appended).  Same formula.
  *   q, out: [num_seqs][num_q_heads][head_dim]; out has q_dtype.
  *   kv_split_len: keys per split-K partition (0 = library choice, else a
- *   positive multiple of 64).  Partitions are fixed by logical positions only,
- *   so results do not depend on physical page placement.
+ *   positive multiple of 64, at most 256 * page_size).  Partitions are fixed
+ *   by logical positions only, so results do not depend on physical page
+ *   placement.
  *   workspace: at least paged_decode_workspace_bytes(...) bytes.
  */
 ckv_status_t paged_decode_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,

@@ -140,7 +140,9 @@ size_t paged_decode_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t *b
   if (check_pool(pool) != CKV_OK || check_batch(pool, batch, 1) != CKV_OK ||
       check_heads(pool, num_q_heads) != CKV_OK)
     return 0;
-  if (kv_split_len < 0 || kv_split_len % 64 != 0) return 0;
+  if (kv_split_len < 0 || kv_split_len % 64 != 0 ||
+      kv_split_len > ckv::decode_max_split_len(pool->page_size))
+    return 0;
   if (batch->num_seqs == 0 || pool->kv_dtype == CKV_F32) return 0;
   return ckv::decode_workspace_bytes(view(pool), view(batch), num_q_heads, kv_split_len);
 }
@@ -154,7 +156,9 @@ ckv_status_t paged_decode_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
   CKV_TRY(check_heads(pool, num_q_heads));
   CKV_TRY(check_attn_dtypes(pool, q_dtype));
   if (!std::isfinite(softmax_scale) || window < 0) return CKV_ERR_INVALID_ARG;
-  if (kv_split_len < 0 || kv_split_len % 64 != 0) return CKV_ERR_INVALID_ARG;
+  if (kv_split_len < 0 || kv_split_len % 64 != 0 ||
+      kv_split_len > ckv::decode_max_split_len(pool->page_size))
+    return CKV_ERR_INVALID_ARG;
   if (batch->num_seqs == 0) return CKV_OK;
   if (!q || !out) return CKV_ERR_INVALID_ARG;
   if (q_dtype == CKV_F32)

@@ -83,4 +83,83 @@ __device__ __forceinline__ float shfl_xor(float v, int mask) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// ------------------------------------------------------------------- LDS
+// LDS is addressed through address-space-3 pointers throughout, so no
+// generic <-> LDS conversion happens at run time.
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4_t;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4_t;
+
+// View of a __shared__ array as an LDS pointer (folds to a constant).
+template <typename T>
+__device__ __forceinline__ lds_u8 *as_lds(T *shared_array) {
+  return (lds_u8 *)(shared_array);
+}
+
+__device__ __forceinline__ u32x2 ds_read_tr16(const lds_u8 *p) {
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)(p));
+  return __builtin_bit_cast(u32x2, v);
+}
+__device__ __forceinline__ u32x4 lds_ld16(const lds_u8 *p) { return *(const lds_u32x4_t *)(p); }
+__device__ __forceinline__ void lds_st16(lds_u8 *p, u32x4 v) { *(lds_u32x4_t *)(p) = v; }
+
+// Read-only tables (block table, fp8 scales) are read through the constant
+// address space so that wave-uniform lookups become scalar loads.
+template <typename T>
+__device__ __forceinline__ T ldc(const T *p, int i) {
+  return ((const __attribute__((address_space(4))) T *)(p))[i];
+}
+
+// Wave-wide 16-byte-per-lane loads from global memory straight into LDS:
+// lane l's 16 bytes land at dst + 16 l (dst wave-uniform, passed in M0).
+// Issued as inline assembly so that the compiler does not track them; the
+// kernels order them explicitly (s_waitcnt vmcnt, then a barrier when other
+// waves read the data; a stage is overwritten only after its readers have
+// passed a barrier or, for a single-wave ring, after the wave has consumed
+// it).
+__device__ __forceinline__ uint32_t lds_offset(const lds_u8 *p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
+}
+
+// The compiler's hazard recognizer cannot see that these asm statements are
+// vector memory instructions, so they carry their own wait states: the base
+// registers are often written by v_readfirstlane right before the load (a
+// VALU write of an SGPR needs 5 wait states before a VMEM instruction reads
+// it), and M0 by an s_mov (an SALU write of M0 needs 1 before an LDS-DMA
+// load).  Without them the load can use a stale base address.
+#define CKV_DMA_WAIT "s_nop 4\n\t"
+
+// Per-lane 64-bit source address.
+__device__ __forceinline__ void dma16(const void *g, lds_u8 *dst) {
+  asm volatile(CKV_DMA_WAIT "global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds_offset(dst))
+               : "memory");
+}
+
+// Wave-uniform 64-bit base (scalar registers) plus a per-lane 32-bit byte
+// offset: no per-lane 64-bit address arithmetic.
+__device__ __forceinline__ void dma16_sv(const void *sbase, uint32_t voff, lds_u8 *dst) {
+  // readfirstlane returns a signed int: widen each half as unsigned so the
+  // low word is not sign-extended into the high word
+  const uint64_t base = (uint64_t)(uintptr_t)sbase;
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)base);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(base >> 32));
+  const uint64_t sb = ((uint64_t)hi << 32) | (uint64_t)lo;
+  asm volatile(CKV_DMA_WAIT "global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sb),
+               "{m0}"(lds_offset(dst))
+               : "memory");
+}
+
+// Sum of two bf16 values packed in a dword, accumulated in fp32.
+__device__ __forceinline__ float add_bf16x2(uint32_t w, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w),
+                                         __builtin_bit_cast(bf16x2, 0x3f803f80u), acc, false);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
 }  // namespace ckv

@@ -31,6 +31,7 @@ hipError_t launch_prefill_bf16(const PoolView &p, const BatchView &b, const void
 
 size_t decode_workspace_bytes(const PoolView &p, const BatchView &b, int h_q, int split_len);
 int decode_split_len(const PoolView &p, const BatchView &b, int h_q, int requested);
+int decode_max_split_len(int page_size);
 hipError_t launch_decode_bf16(const PoolView &p, const BatchView &b, const void *q, int h_q,
                               float scale, int window, int split_len, void *out, void *ws,
                               size_t ws_bytes, hipStream_t s);
