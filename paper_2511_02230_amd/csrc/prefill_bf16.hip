@@ -364,8 +364,12 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   __shared__ __attribute__((aligned(1024))) uint8_t cvt[FP8 ? 2 * C::BLK : 16];
   lds_u8 *const stages[3] = {as_lds(st0), as_lds(st1), as_lds(st2)};
 
-  const int tile = a.tiles - 1 - (int)blockIdx.x;  // later (costlier) tiles first
-  const int g = blockIdx.y;
+  // grid (H_kv, tiles, B): workgroups are dealt to the XCDs round-robin in
+  // linear order, so with 8 KV heads every row tile of one (sequence, KV
+  // head) lands on the same XCD, next to its neighbours in time, and the
+  // tiles streaming the same K/V share that XCD's L2
+  const int g = blockIdx.x;
+  const int tile = a.tiles - 1 - (int)blockIdx.y;  // later (costlier) tiles first
   const int b = blockIdx.z;
   const int q0 = a.cu[b];
   const int n = a.cu[b + 1] - q0;
@@ -449,7 +453,7 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
 
 template <int D, int BN, int NS, bool FP8>
 hipError_t launch(const PrefillArgs &a, int ps, int h_kv, int num_seqs, hipStream_t s) {
-  dim3 grid(a.tiles, h_kv, num_seqs);
+  dim3 grid(h_kv, a.tiles, num_seqs);
   if (ps == 16)
     hipLaunchKernelGGL((prefill_kernel<D, BN, NS, FP8, 16>), grid, dim3(kThreads), 0, s, a);
   else
@@ -480,6 +484,7 @@ hipError_t launch_prefill_bf16(const PoolView &p, const BatchView &b, const void
   a.window = window;
   const long long rows = (long long)b.max_q * a.group;
   a.tiles = (int)((rows + kRows - 1) / kRows);
+  if (a.tiles > 65535) return hipErrorInvalidConfiguration;  // grid.y limit
   const bool fp8 = p.kv_dtype == 2;
   switch (p.d) {
     case 64:
