@@ -65,6 +65,7 @@ template <int D, int BN, int NS, bool FP8, int PS>
 struct Cfg {
   static constexpr int ROW = D * 2;                    // bf16 bytes per key row in LDS
   static constexpr int CH = D / 8;                     // 16-byte chunks per bf16 row
+  static constexpr int BN_ = BN;                       // keys per block
   static constexpr int BLK = BN * ROW;                 // bf16 bytes of one K (or V) block
   static constexpr int RAW_ROW = FP8 ? D : D * 2;      // pool bytes per key row
   static constexpr int RCH = RAW_ROW / 16;             // 16-byte chunks per pool row
@@ -97,74 +98,84 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// Which block rows / tensor the i-th load of this wave covers.
-template <class C>
-__device__ __forceinline__ void load_slot(int wave, int i, int &tensor, int &r) {
-  const int idx = wave * C::DPW + i;  // 0 .. 2*DMA_PER_TENSOR-1
-  tensor = idx / C::DMA_PER_TENSOR;   // 0 = K, 1 = V
-  r = idx % C::DMA_PER_TENSOR;
-}
-
-// Per-lane byte offset, relative to the first row of load i, of the 16
-// bytes this lane fetches; fixed for the kernel.  Lane l lands in LDS slot
-// l of the load (row l / RCH, chunk slot l % RCH) and fetches the chunk that
-// the swizzle assigns to that slot.
-template <class C, bool FP8>
+// Load plan: wave w fills half h = w & 1 of tensor t = w >> 1 (0 = K, 1 = V)
+// of each block, i.e. rows h BN/2 .. h BN/2 + BN/2 - 1, with DPW wave-wide
+// 1-KB loads of RPD rows each.  Those rows span NPW pages (DPP loads each),
+// so a block costs the wave NPW page-table reads and NPW scalar bases; the
+// per-lane part of every load's address is fixed for the whole kernel.
+// Per-lane byte offset of load i, relative to the scalar base of its page
+// (the page's first row covered by this wave).  Lane l lands in LDS slot l of
+// the load (row l / RCH, chunk slot l % RCH) and fetches the chunk that the
+// swizzle assigns to that slot.
+template <class C, int PS, bool FP8>
 __device__ __forceinline__ void lane_offsets(uint32_t (&loff)[C::DPW]) {
+  constexpr int HROWS = C::RAW_BLK / 2 / C::RAW_ROW;
+  constexpr int NPW = HROWS > PS ? HROWS / PS : 1;
+  constexpr int DPP = C::DPW / NPW;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  const int t = wave >> 1, h = wave & 1;
 #pragma unroll
   for (int i = 0; i < C::DPW; ++i) {
-    int tensor, r;
-    load_slot<C>(wave, i, tensor, r);
-    const int row = r * C::RPD + lane / C::RCH;
+    const int row = h * HROWS + i * C::RPD + lane / C::RCH;  // row within the block
     const int slot = lane % C::RCH;
     int chunk = slot;
-    if constexpr (!FP8) chunk = slot ^ (tensor == 0 ? swz_k<C::CH>(row) : swz_v<C::CH>(row));
-    loff[i] = (uint32_t)((lane / C::RCH) * C::RAW_ROW + chunk * 16);
+    if constexpr (!FP8) chunk = slot ^ (t == 0 ? swz_k<C::CH>(row) : swz_v<C::CH>(row));
+    loff[i] = (uint32_t)(((i % DPP) * C::RPD + lane / C::RCH) * C::RAW_ROW + chunk * 16);
   }
 }
 
-// Page id of each load this wave issues for the block starting at kbase
-// (scalar loads through the constant address space).
+// Page ids of the NPW pages this wave loads for the block at kbase (scalar
+// loads through the constant address space).  Pages are looked up by the
+// first row the wave covers in them, clamped to kv_end - 1.
 template <class C, int PS>
 __device__ __forceinline__ void block_pages(const int32_t *bt, int kbase, int kv_end, int (&pg)[C::DPW]) {
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  constexpr int HROWS = C::RAW_BLK / 2 / C::RAW_ROW;
+  constexpr int NPW = HROWS > PS ? HROWS / PS : 1;
+  const int h = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & 1;
 #pragma unroll
-  for (int i = 0; i < C::DPW; ++i) {
-    int tensor, r;
-    load_slot<C>(wave, i, tensor, r);
-    const int kp0 = min(kbase + r * C::RPD, kv_end - 1);
-    pg[i] = ldc(bt, __builtin_amdgcn_readfirstlane(kp0 / PS));
+  for (int p = 0; p < NPW; ++p) {
+    const int key = min(kbase + h * HROWS + p * PS, kv_end - 1);
+    pg[p] = ldc(bt, key / PS);
   }
 }
 
 // Issue this wave's loads of one block into an LDS stage.  Rows at or beyond
 // kv_end (last block only) are redirected to row kv_end - 1: valid, finite
-// data in the same page as the load's first row, which the causal mask
-// removes.
+// data in the same page as the load's first row (or that row's page), which
+// the causal mask removes.
 template <class C, int PS, bool FP8>
-__device__ __forceinline__ void issue_block(const PrefillArgs &a, int g, int kbase, int kv_end,
-                                            const int (&pg)[C::DPW], const uint32_t (&loff)[C::DPW],
-                                            lds_u8 *stage) {
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ void issue_block(const PrefillArgs &a, const int32_t *bt, int g, int kbase,
+                                            int kv_end, const int (&pg)[C::DPW],
+                                            const uint32_t (&loff)[C::DPW], lds_u8 *stage) {
+  constexpr int HROWS = C::RAW_BLK / 2 / C::RAW_ROW;
+  constexpr int NPW = HROWS > PS ? HROWS / PS : 1;
+  constexpr int DPP = C::DPW / NPW;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int t = wave >> 1, h = wave & 1;
+  const uint8_t *tens = t == 0 ? a.k : a.v;
   const size_t page_stride = (size_t)a.h_kv * PS * C::RAW_ROW;
   const size_t head_off = (size_t)g * PS * C::RAW_ROW;
-  const bool tail = kbase + (int)(C::DMA_PER_TENSOR * C::RPD) > kv_end;
+  lds_u8 *wdst = stage + t * C::RAW_BLK + h * (C::RAW_BLK / 2);
+  if (kbase + C::BN_ <= kv_end) {
 #pragma unroll
-  for (int i = 0; i < C::DPW; ++i) {
-    int tensor, r;
-    load_slot<C>(wave, i, tensor, r);
-    const int kp0 = kbase + r * C::RPD;
-    const uint8_t *page_base = (tensor == 0 ? a.k : a.v) + (size_t)pg[i] * page_stride + head_off;
-    lds_u8 *dst = stage + tensor * C::RAW_BLK + r * 1024;
-    if (!tail) {
-      dma16_sv(page_base + (size_t)(kp0 % PS) * C::RAW_ROW, loff[i], dst);
-    } else {
-      const int kp = min(kp0 + lane / C::RCH, kv_end - 1);
+    for (int p = 0; p < NPW; ++p) {
+      const int key = kbase + h * HROWS + p * PS;
+      const uint8_t *base = tens + (size_t)pg[p] * page_stride + head_off + (size_t)(key % PS) * C::RAW_ROW;
+#pragma unroll
+      for (int i = p * DPP; i < (p + 1) * DPP; ++i) dma16_sv(base, loff[i], wdst + i * 1024);
+    }
+  } else {
+    // last block: per-load page of its first row (clamped), per-lane clamp
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < C::DPW; ++i) {
+      const int kf = min(kbase + h * HROWS + i * C::RPD, kv_end - 1);
+      const int pgi = ldc(bt, kf / PS);
+      const uint8_t *base = tens + (size_t)pgi * page_stride + head_off;
+      const int kp = min(kbase + h * HROWS + i * C::RPD + lane / C::RCH, kv_end - 1);
       const uint32_t voff = (uint32_t)((kp % PS) * C::RAW_ROW) + (loff[i] % C::RAW_ROW);
-      dma16_sv(page_base, voff, dst);
+      dma16_sv(base, voff, wdst + i * 1024);
     }
   }
 }
@@ -229,7 +240,7 @@ __device__ __forceinline__ void block_step(const PrefillArgs &a, const int32_t *
   }
   lds_barrier();
   if (issue)
-    issue_block<C, PS, FP8>(a, T.g, kbase + (NS - 1) * BN, T.kv_end, T.pg, T.loff,
+    issue_block<C, PS, FP8>(a, bt, T.g, kbase + (NS - 1) * BN, T.kv_end, T.pg, T.loff,
                             stages[(U + NS - 1) % NS]);
   const lds_u8 *kb;
   const lds_u8 *vb;
@@ -394,8 +405,11 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   T.ipos = rvalid ? P + t : -1;
   const size_t qrow = ((size_t)(q0 + t) * a.h_q + (size_t)g * G + hh) * D;
 
-  const int t_first = R0 / G;
-  const int t_last = min(n - 1, (R0 + kRows - 1) / G);
+  // workgroup-uniform bounds, pinned to scalar registers (the integer
+  // divisions would otherwise leave them in vector registers and drag the
+  // whole load-address computation onto the VALU)
+  const int t_first = __builtin_amdgcn_readfirstlane(R0 / G);
+  const int t_last = __builtin_amdgcn_readfirstlane(min(n - 1, (R0 + kRows - 1) / G));
   T.i_min = P + t_first;
   T.i_max = P + t_last;
   T.kv_end = T.i_max + 1;
@@ -405,13 +419,13 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   const int kb_end = (T.kv_end + BN - 1) / BN;
   T.nblk = kb_end - T.kb_begin;
 
-  lane_offsets<C, FP8>(T.loff);
+  lane_offsets<C, PS, FP8>(T.loff);
   // prologue: the first NS-1 blocks in flight before anything else
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s) {
     if (s < T.nblk) {
       block_pages<C, PS>(bt, (T.kb_begin + s) * BN, T.kv_end, T.pg);
-      issue_block<C, PS, FP8>(a, g, (T.kb_begin + s) * BN, T.kv_end, T.pg, T.loff, stages[s]);
+      issue_block<C, PS, FP8>(a, bt, g, (T.kb_begin + s) * BN, T.kv_end, T.pg, T.loff, stages[s]);
     }
   }
 
