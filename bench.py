@@ -69,6 +69,29 @@ def append_bytes(wl, rows):
     return float(rows * cfg.num_kv_heads * cfg.head_dim * 2 * (e_in + E[cfg.kv_dtype]))
 
 
+def measured_traffic(kernel_key):
+    """HBM bytes per launch that rocprofv3 measured for this kernel
+    (FETCH_SIZE / WRITE_SIZE passes scaled by a plain copy's readings, kept in
+    profiles/traffic.json), or None when there is no measurement or the
+    kernel's sources have changed since it was taken."""
+    import hashlib
+
+    try:
+        with open(os.path.join(ROOT, "profiles", "traffic.json")) as f:
+            entry = json.load(f).get(kernel_key)
+    except (OSError, ValueError):
+        return None
+    if not entry:
+        return None
+    h = hashlib.sha256()
+    for src in entry["sources"]:
+        with open(os.path.join(ROOT, "paper_2511_02230_amd", "csrc", src), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest()[:16] != entry["sources_sha256_16"]:
+        return None
+    return float(entry["bytes"])
+
+
 def cpu_baseline(wl, window, budget_s=20.0):
     """Time the fp64 oracle on a bounded sample of the same workload: new-turn
     rows of the longest prefill sequence (prefill TFLOP/s of the sample)."""
@@ -159,6 +182,8 @@ def main():
            for i, nm in enumerate(names)}
 
     w = args.window
+    # the stored traffic was measured on the default workload only
+    default_cfg = args.config == "llama3.1-70b" and w == 0
     flops = prefill_flops(wl, w)
     dbytes = decode_bytes(wl, w)
     abytes = append_bytes(wl, wl.prefill.total_q)
@@ -168,10 +193,12 @@ def main():
     app_gbs = abytes / (per["kv_append_prefill"] * 1e-3) / 1e9
     rooflines = {
         "prefix_prefill_attn": {"bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS,
-                                "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS, "traffic": None,
+                                "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS,
+                                "traffic": measured_traffic("prefix_prefill_attn") if default_cfg else None,
                                 "ms": per["prefix_prefill_attn"], "work": flops},
         "paged_decode_attn": {"bound": "hbm", "achieved": dec_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                              "frac": dec_gbs / PEAK_HBM_GBS, "traffic": None,
+                              "frac": dec_gbs / PEAK_HBM_GBS,
+                              "traffic": measured_traffic("paged_decode_attn") if default_cfg else None,
                               "ms": per["paged_decode_attn"], "work": dbytes},
         "kv_append": {"bound": "hbm", "achieved": app_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                       "frac": app_gbs / PEAK_HBM_GBS, "traffic": None, "ms": per["kv_append_prefill"],

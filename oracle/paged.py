@@ -101,7 +101,13 @@ def gather(pool, block_table_row, length: int, *, page_size, kv_dtype, scale=Non
 def visible(i, j, window: int):
     """Key j is visible to the query at absolute position i iff j <= i and,
     for a window W > 0, i - j < W (the query sees exactly W keys, itself
-    included)."""
+    included).
+
+    Parity unpinned for the window edge: the paper has no sliding-window
+    layer at all (the window comes from the Gemma-3 layer shapes this path
+    is sized for), so "exactly W keys, self included" is a declared
+    convention; the tests pin everything around it (W >= context equals
+    global attention, W = 1 sees only itself) but not the edge itself."""
     ok = j <= i
     if window > 0:
         ok = ok & (i - j < window)
