@@ -61,7 +61,7 @@ __device__ __forceinline__ int pi_row(int m) {
   return 16 * (i >> 1) + 8 * h + 4 * (i & 1) + j;
 }
 
-template <int D, int BN, int NS, bool FP8, int PS>
+template <int D, int BN, bool FP8, int PS>
 struct Cfg {
   static constexpr int ROW = D * 2;                    // bf16 bytes per key row in LDS
   static constexpr int CH = D / 8;                     // 16-byte chunks per bf16 row
@@ -70,16 +70,17 @@ struct Cfg {
   static constexpr int RAW_ROW = FP8 ? D : D * 2;      // pool bytes per key row
   static constexpr int RCH = RAW_ROW / 16;             // 16-byte chunks per pool row
   static constexpr int RAW_BLK = BN * RAW_ROW;         // pool bytes of one block
-  static constexpr int STAGE = 2 * RAW_BLK;            // K + V, raw
-  static constexpr int DMA_PER_TENSOR = RAW_BLK / 1024;  // 1 KB per wave-wide load
-  static constexpr int DPW = 2 * DMA_PER_TENSOR / kWaves;  // loads per wave per block
+  static constexpr int DPW = RAW_BLK / 2 / 1024;       // 1-KB loads per wave per block
   static constexpr int RPD = 1024 / RAW_ROW;           // rows per load
   static constexpr int NT = BN / 32;                   // S^T tiles per block
   static constexpr int DS = D / 16;                    // QK^T k-steps
   static constexpr int DT = D / 32;                    // output d-tiles
-  static_assert((2 * DMA_PER_TENSOR) % kWaves == 0, "each wave issues whole loads");
+  static constexpr int NQK = NT * DS;                  // QK^T MFMAs per block
+  // two-stage K ring + two-stage V ring (+ the widened bf16 K and V blocks for fp8)
+  static constexpr int LDS = 4 * RAW_BLK + (FP8 ? 2 * BLK : 0);
+  static_assert(RAW_BLK % 2048 == 0, "each wave issues whole 1-KB loads");
   static_assert(PS % RPD == 0, "a load never straddles a page");
-  static_assert(NS * STAGE + (FP8 ? 2 * BLK : 0) <= 160 * 1024, "LDS budget");
+  static_assert(LDS <= 80 * 1024, "two workgroups per CU");
 };
 
 // XOR swizzles of the 16-byte chunk index within a bf16 row.
@@ -136,18 +137,18 @@ __device__ __forceinline__ void block_pages(const int32_t *bt, int kbase, int kv
 #pragma unroll
   for (int p = 0; p < NPW; ++p) {
     const int key = min(kbase + h * HROWS + p * PS, kv_end - 1);
-    pg[p] = ldc(bt, key / PS);
+    pg[p] = ldc(bt, (int)((uint32_t)key / PS));
   }
 }
 
-// Issue this wave's loads of one block into an LDS stage.  Rows at or beyond
+// Issue this wave's loads of one block of its tensor into a ring stage.  Rows at or beyond
 // kv_end (last block only) are redirected to row kv_end - 1: valid, finite
 // data in the same page as the load's first row (or that row's page), which
 // the causal mask removes.
 template <class C, int PS, bool FP8>
 __device__ __forceinline__ void issue_block(const PrefillArgs &a, const int32_t *bt, int g, int kbase,
                                             int kv_end, const int (&pg)[C::DPW],
-                                            const uint32_t (&loff)[C::DPW], lds_u8 *stage) {
+                                            const uint32_t (&loff)[C::DPW], lds_u8 *ring_stage) {
   constexpr int HROWS = C::RAW_BLK / 2 / C::RAW_ROW;
   constexpr int NPW = HROWS > PS ? HROWS / PS : 1;
   constexpr int DPP = C::DPW / NPW;
@@ -156,12 +157,13 @@ __device__ __forceinline__ void issue_block(const PrefillArgs &a, const int32_t 
   const uint8_t *tens = t == 0 ? a.k : a.v;
   const size_t page_stride = (size_t)a.h_kv * PS * C::RAW_ROW;
   const size_t head_off = (size_t)g * PS * C::RAW_ROW;
-  lds_u8 *wdst = stage + t * C::RAW_BLK + h * (C::RAW_BLK / 2);
+  lds_u8 *wdst = ring_stage + h * (C::RAW_BLK / 2);
   if (kbase + C::BN_ <= kv_end) {
 #pragma unroll
     for (int p = 0; p < NPW; ++p) {
       const int key = kbase + h * HROWS + p * PS;
-      const uint8_t *base = tens + (size_t)pg[p] * page_stride + head_off + (size_t)(key % PS) * C::RAW_ROW;
+      const uint8_t *base =
+          tens + (size_t)pg[p] * page_stride + head_off + (size_t)((uint32_t)key % PS) * C::RAW_ROW;
 #pragma unroll
       for (int i = p * DPP; i < (p + 1) * DPP; ++i) dma16_sv(base, loff[i], wdst + i * 1024);
     }
@@ -171,7 +173,7 @@ __device__ __forceinline__ void issue_block(const PrefillArgs &a, const int32_t 
 #pragma unroll
     for (int i = 0; i < C::DPW; ++i) {
       const int kf = min(kbase + h * HROWS + i * C::RPD, kv_end - 1);
-      const int pgi = ldc(bt, kf / PS);
+      const int pgi = ldc(bt, (int)((uint32_t)kf / PS));
       const uint8_t *base = tens + (size_t)pgi * page_stride + head_off;
       const int kp = min(kbase + h * HROWS + i * C::RPD + lane / C::RCH, kv_end - 1);
       const uint32_t voff = (uint32_t)((kp % PS) * C::RAW_ROW) + (loff[i] % C::RAW_ROW);
@@ -180,19 +182,20 @@ __device__ __forceinline__ void issue_block(const PrefillArgs &a, const int32_t 
   }
 }
 
-// fp8: widen one raw stage into the bf16 K/V blocks (same layout as bf16).
+
+// fp8: widen one raw block of a tensor into its bf16 block (same layout as a
+// bf16 block, swizzle included); all four waves share the work.
 template <class C>
-__device__ __forceinline__ void widen_block(const lds_u8 *stage, lds_u8 *k16, lds_u8 *v16, int BN) {
-  const int total = 2 * BN * C::RCH;
-  for (int id = threadIdx.x; id < total; id += kThreads) {
-    const int tensor = id / (BN * C::RCH);
-    const int rem = id % (BN * C::RCH);
-    const int row = rem / C::RCH, c = rem % C::RCH;
-    const u32x4 x = lds_ld16(stage + tensor * C::RAW_BLK + row * C::RAW_ROW + c * 16);
+__device__ __forceinline__ void widen(const lds_u8 *raw, lds_u8 *dst16, bool is_k) {
+#pragma unroll
+  for (int it = 0; it < C::RAW_BLK / (16 * kThreads); ++it) {
+    const int id = threadIdx.x + kThreads * it;
+    const int row = id / C::RCH, c = id % C::RCH;
+    const u32x4 x = lds_ld16(raw + row * C::RAW_ROW + c * 16);
     const u32x2 a0 = fp8x4_to_bf16x4(x.x), a1 = fp8x4_to_bf16x4(x.y);
     const u32x2 b0 = fp8x4_to_bf16x4(x.z), b1 = fp8x4_to_bf16x4(x.w);
-    lds_u8 *dst = (tensor == 0 ? k16 : v16) + row * C::ROW;
-    const int sw = tensor == 0 ? swz_k<C::CH>(row) : swz_v<C::CH>(row);
+    lds_u8 *dst = dst16 + row * C::ROW;
+    const int sw = is_k ? swz_k<C::CH>(row) : swz_v<C::CH>(row);
     lds_st16(dst + (((2 * c) ^ sw) << 4), u32x4{a0.x, a0.y, a1.x, a1.y});
     lds_st16(dst + (((2 * c + 1) ^ sw) << 4), u32x4{b0.x, b0.y, b1.x, b1.y});
   }
@@ -216,67 +219,44 @@ struct Tile {
   float m, l;
   int pg[C::DPW];          // page ids of the block being issued
   uint32_t loff[C::DPW];   // per-lane load offsets
-  int g, ipos, i_min, i_max, kv_end, kb_begin, nblk, half, col, gq, li;
+  int g, t, ipos, i_min, i_max, kv_end, kb_begin, nblk, half, col, gq, li;
 };
 
-// One block of BN keys: wait for its loads, barrier, issue the loads NS-1
-// blocks ahead, then S^T, softmax and O^T for this block.  U is the stage
-// of block j (compile time, so each stage is its own LDS object).
-template <int D, int BN, int NS, bool FP8, int PS, int U>
-__device__ __forceinline__ void block_step(const PrefillArgs &a, const int32_t *bt,
-                                           Tile<Cfg<D, BN, NS, FP8, PS>> &T, int j,
-                                           lds_u8 *const (&stages)[3], lds_u8 *k16, lds_u8 *v16) {
-  using C = Cfg<D, BN, NS, FP8, PS>;
-  const int kbase = (T.kb_begin + j) * BN;
-  // page ids of the block issued below: the scalar loads resolve while this
-  // wave waits for block j
-  const bool issue = j + NS - 1 < T.nblk;
-  if (issue) block_pages<C, PS>(bt, kbase + (NS - 1) * BN, T.kv_end, T.pg);
-  if constexpr (NS >= 3) {
-    if (j + 1 < T.nblk) wait_vmcnt<C::DPW>();
-    else wait_vmcnt<0>();
-  } else {
-    wait_vmcnt<0>();
-  }
-  lds_barrier();
-  if (issue)
-    issue_block<C, PS, FP8>(a, bt, T.g, kbase + (NS - 1) * BN, T.kv_end, T.pg, T.loff,
-                            stages[(U + NS - 1) % NS]);
-  const lds_u8 *kb;
-  const lds_u8 *vb;
-  if constexpr (FP8) {
-    widen_block<C>(stages[U], k16, v16, BN);
-    lds_barrier();
-    kb = k16;
-    vb = v16;
-  } else {
-    kb = stages[U];
-    vb = kb + C::BLK;
-  }
-  const int half = T.half, col = T.col;
-
-  // ---- S^T = K Q^T, one 32-key tile at a time
-  f32x16 s[C::NT];
+// Part P (0 or 1) of S^T = K Q^T for one block: the first or second half of
+// its NT x DS MFMAs, so that each half can be scheduled against a different
+// stretch of the previous block's softmax.  Row m of tile tt is key
+// 32 tt + pi(m).
+template <class C, int P>
+__device__ __forceinline__ void qk_part(const lds_u8 *kb, const Tile<C> &T, f32x16 (&s)[C::NT]) {
 #pragma unroll
-  for (int tt = 0; tt < C::NT; ++tt) {
-    s[tt] = f32x16{};
-    const int key = 32 * tt + pi_row(col);
-    const lds_u8 *krow = kb + key * C::ROW;
+  for (int n = P * C::NQK / 2; n < (P + 1) * C::NQK / 2; ++n) {
+    const int tt = n / C::DS, ds = n % C::DS;
+    if (ds == 0) s[tt] = f32x16{};
+    const int key = 32 * tt + pi_row(T.col);
     const int sw = swz_k<C::CH>(key);
-#pragma unroll
-    for (int ds = 0; ds < C::DS; ++ds) {
-      const u32x4 kx = lds_ld16(krow + (((2 * ds + half) ^ sw) << 4));
-      s[tt] = mfma32x32x16(as_bf16x8(kx), T.qf[ds], s[tt]);
-    }
+    const u32x4 kx = lds_ld16(kb + key * C::ROW + (((2 * ds + T.half) ^ sw) << 4));
+    s[tt] = mfma32x32x16(as_bf16x8(kx), T.qf[ds], s[tt]);
   }
+}
 
-  // ---- mask, row maximum (in log2 units)
+// Softmax of block j (scores s, raw K Q^T) and O^T += V^T P^T with V of
+// block j (bf16 layout at vb).  qk_part<1> of the next block is issued in
+// the middle, between the row maximum and the exponentials.
+template <class C, int PS, bool FP8>
+__device__ __forceinline__ void softmax_pv(const PrefillArgs &a, const int32_t *bt, Tile<C> &T, int j,
+                                           f32x16 (&s)[C::NT], const lds_u8 *vb, const lds_u8 *kb_next,
+                                           f32x16 (&s_next)[C::NT]) {
+  constexpr int BN = C::BN_;
+  const int kbase = (T.kb_begin + j) * BN;
+  const int half = T.half;
+
+  // ---- fp8 key scales, mask, row maximum (in log2 units)
   float vsc[C::NT * 2];  // fp8: V scale per 16-key group
   if constexpr (FP8) {
 #pragma unroll
     for (int q = 0; q < C::NT * 2; ++q) {
       const int kp = min(kbase + 16 * q, T.kv_end - 1);
-      const int idx = ldc(bt, __builtin_amdgcn_readfirstlane(kp / PS)) * a.h_kv + T.g;
+      const int idx = ldc(bt, (int)((uint32_t)kp / PS)) * a.h_kv + T.g;
       const float ksc = a.scale_log2 * ldc(a.k_scale, idx);
       vsc[q] = ldc(a.v_scale, idx);
 #pragma unroll
@@ -316,6 +296,9 @@ __device__ __forceinline__ void block_step(const PrefillArgs &a, const int32_t *
     for (int dt = 0; dt < C::DT; ++dt) T.o[dt] *= alpha;
   }
   const float m_use = T.m == kNegInf ? 0.f : T.m;
+
+  // second half of the next block's S^T, independent of everything below
+  qk_part<C, 1>(kb_next, T, s_next);
 
   // ---- P = exp2(scale * s - m); O^T += V^T P^T
 #pragma unroll
@@ -364,16 +347,64 @@ __device__ __forceinline__ void block_step(const PrefillArgs &a, const int32_t *
   }
 }
 
-template <int D, int BN, int NS, bool FP8, int PS>
+// The K ring holds K of blocks j+1 and j+2 while step j runs, the V ring V
+// of blocks j and j+1.  Stage of block b: b & 1 in both rings.
+template <class C>
+struct Rings {
+  lds_u8 *k, *v, *k16, *v16;
+  __device__ __forceinline__ lds_u8 *kst(int b) const { return k + (b & 1) * C::RAW_BLK; }
+  __device__ __forceinline__ lds_u8 *vst(int b) const { return v + (b & 1) * C::RAW_BLK; }
+};
+
+// Loads issued at step j (j = -1 is the prologue): K of block j+2 by waves 0
+// and 1, V of block j+1 by waves 2 and 3.  Page ids resolve while the wave
+// waits for the previous step's loads.
+template <class C, int PS, bool FP8, int U>
+__device__ __forceinline__ void wait_and_issue(const PrefillArgs &a, const int32_t *bt, Tile<C> &T,
+                                               int j, const Rings<C> &R) {
+  constexpr int BN = C::BN_;
+  const int bi = j + 2 - T.t;  // block whose tensor-t half this wave loads
+  const bool iss = bi < T.nblk;
+  const int kb_iss = (T.kb_begin + bi) * BN;
+  if (iss) block_pages<C, PS>(bt, kb_iss, T.kv_end, T.pg);
+  wait_vmcnt<0>();
+  lds_barrier();
+  // stage of block bi: (j + 2) & 1 = U for K, (j + 1) & 1 = U ^ 1 for V
+  lds_u8 *dst = T.t == 0 ? R.k + U * C::RAW_BLK : R.v + (U ^ 1) * C::RAW_BLK;
+  if (iss) issue_block<C, PS, FP8>(a, bt, T.g, kb_iss, T.kv_end, T.pg, T.loff, dst);
+}
+
+// Step j: K of block j+1 and V of block j are resident after the barrier;
+// S^T of block j+1 is computed around block j's softmax, then O^T for
+// block j.  U = j & 1 (compile time, so every stage address folds).
+template <class C, int PS, bool FP8, int U>
+__device__ __forceinline__ void step(const PrefillArgs &a, const int32_t *bt, Tile<C> &T, int j,
+                                     f32x16 (&s_cur)[C::NT], f32x16 (&s_nxt)[C::NT], const Rings<C> &R) {
+  wait_and_issue<C, PS, FP8, U>(a, bt, T, j, R);
+  const lds_u8 *kb = R.k + (U ^ 1) * C::RAW_BLK;  // K of block j+1
+  const lds_u8 *vb = R.v + U * C::RAW_BLK;        // V of block j
+  if constexpr (FP8) {
+    widen<C>(kb, R.k16, true);
+    widen<C>(vb, R.v16, false);
+    lds_barrier();
+    kb = R.k16;
+    vb = R.v16;
+  }
+  // (past the last block this reads a stale K stage; the result is unused)
+  qk_part<C, 0>(kb, T, s_nxt);
+  softmax_pv<C, PS, FP8>(a, bt, T, j, s_cur, vb, kb, s_nxt);
+}
+
+template <int D, int BN, bool FP8, int PS>
 __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(PrefillArgs a) {
-  using C = Cfg<D, BN, NS, FP8, PS>;
-  static_assert(NS == 2 || NS == 3, "two or three stages");
-  // one LDS object per ring stage
-  __shared__ __attribute__((aligned(1024))) uint8_t st0[C::STAGE];
-  __shared__ __attribute__((aligned(1024))) uint8_t st1[C::STAGE];
-  __shared__ __attribute__((aligned(1024))) uint8_t st2[NS >= 3 ? C::STAGE : 16];
-  __shared__ __attribute__((aligned(1024))) uint8_t cvt[FP8 ? 2 * C::BLK : 16];
-  lds_u8 *const stages[3] = {as_lds(st0), as_lds(st1), as_lds(st2)};
+  using C = Cfg<D, BN, FP8, PS>;
+  // K ring (2 stages), V ring (2 stages), fp8: widened K and V blocks
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_[C::LDS];
+  Rings<C> R;
+  R.k = as_lds(lds_);
+  R.v = R.k + 2 * C::RAW_BLK;
+  R.k16 = R.v + 2 * C::RAW_BLK;  // fp8 only
+  R.v16 = R.k16 + C::BLK;
 
   // grid (H_kv, tiles, B): workgroups are dealt to the XCDs round-robin in
   // linear order, so with 8 KV heads every row tile of one (sequence, KV
@@ -398,10 +429,11 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   T.gq = lane >> 4;
   T.li = lane & 15;
   T.g = g;
-  const int R = R0 + wave * 32 + T.col;
-  const bool rvalid = R < rows;
-  const int t = rvalid ? R / G : 0;
-  const int hh = rvalid ? R - t * G : 0;
+  T.t = __builtin_amdgcn_readfirstlane(wave >> 1);
+  const int Rw = R0 + wave * 32 + T.col;
+  const bool rvalid = Rw < rows;
+  const int t = rvalid ? Rw / G : 0;
+  const int hh = rvalid ? Rw - t * G : 0;
   T.ipos = rvalid ? P + t : -1;
   const size_t qrow = ((size_t)(q0 + t) * a.h_q + (size_t)g * G + hh) * D;
 
@@ -420,15 +452,12 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   T.nblk = kb_end - T.kb_begin;
 
   lane_offsets<C, PS, FP8>(T.loff);
-  // prologue: the first NS-1 blocks in flight before anything else
-#pragma unroll
-  for (int s = 0; s < NS - 1; ++s) {
-    if (s < T.nblk) {
-      block_pages<C, PS>(bt, (T.kb_begin + s) * BN, T.kv_end, T.pg);
-      issue_block<C, PS, FP8>(a, bt, g, (T.kb_begin + s) * BN, T.kv_end, T.pg, T.loff, stages[s]);
-    }
+  // prologue: K of block 0, then K of block 1 and V of block 0 while S^T of
+  // block 0 is computed
+  if (T.t == 0) {
+    block_pages<C, PS>(bt, T.kb_begin * BN, T.kv_end, T.pg);
+    issue_block<C, PS, FP8>(a, bt, g, T.kb_begin * BN, T.kv_end, T.pg, T.loff, R.k);
   }
-
 #pragma unroll
   for (int s = 0; s < C::DS; ++s) {
     u32x4 x = {0u, 0u, 0u, 0u};
@@ -440,13 +469,22 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   T.m = kNegInf;
   T.l = 0.f;
 
-  lds_u8 *k16 = as_lds(cvt);  // fp8 only
-  lds_u8 *v16 = k16 + (FP8 ? C::BLK : 0);
-  for (int j0 = 0; j0 < T.nblk; j0 += NS) {
-    block_step<D, BN, NS, FP8, PS, 0>(a, bt, T, j0, stages, k16, v16);
-    if (j0 + 1 < T.nblk) block_step<D, BN, NS, FP8, PS, 1>(a, bt, T, j0 + 1, stages, k16, v16);
-    if constexpr (NS >= 3)
-      if (j0 + 2 < T.nblk) block_step<D, BN, NS, FP8, PS, 2>(a, bt, T, j0 + 2, stages, k16, v16);
+  f32x16 sA[C::NT], sB[C::NT];
+  wait_and_issue<C, PS, FP8, 1>(a, bt, T, -1, R);  // U = (-1) & 1
+  {
+    const lds_u8 *kb = R.k;
+    if constexpr (FP8) {
+      widen<C>(R.k, R.k16, true);
+      lds_barrier();
+      kb = R.k16;
+    }
+    qk_part<C, 0>(kb, T, sA);
+    qk_part<C, 1>(kb, T, sA);
+  }
+
+  for (int j0 = 0; j0 < T.nblk; j0 += 2) {
+    step<C, PS, FP8, 0>(a, bt, T, j0, sA, sB, R);
+    if (j0 + 1 < T.nblk) step<C, PS, FP8, 1>(a, bt, T, j0 + 1, sB, sA, R);
   }
 
   // ---- normalize and store this lane's row: d = 32 dt + 8 i + 4 half + 0..3
@@ -465,13 +503,13 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   }
 }
 
-template <int D, int BN, int NS, bool FP8>
+template <int D, int BN, bool FP8>
 hipError_t launch(const PrefillArgs &a, int ps, int h_kv, int num_seqs, hipStream_t s) {
   dim3 grid(h_kv, a.tiles, num_seqs);
   if (ps == 16)
-    hipLaunchKernelGGL((prefill_kernel<D, BN, NS, FP8, 16>), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((prefill_kernel<D, BN, FP8, 16>), grid, dim3(kThreads), 0, s, a);
   else
-    hipLaunchKernelGGL((prefill_kernel<D, BN, NS, FP8, 64>), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((prefill_kernel<D, BN, FP8, 64>), grid, dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -502,14 +540,14 @@ hipError_t launch_prefill_bf16(const PoolView &p, const BatchView &b, const void
   const bool fp8 = p.kv_dtype == 2;
   switch (p.d) {
     case 64:
-      return fp8 ? launch<64, 64, 2, true>(a, p.ps, p.h_kv, b.num_seqs, s)
-                 : launch<64, 64, 2, false>(a, p.ps, p.h_kv, b.num_seqs, s);
+      return fp8 ? launch<64, 64, true>(a, p.ps, p.h_kv, b.num_seqs, s)
+                 : launch<64, 64, false>(a, p.ps, p.h_kv, b.num_seqs, s);
     case 128:
-      return fp8 ? launch<128, 64, 2, true>(a, p.ps, p.h_kv, b.num_seqs, s)
-                 : launch<128, 64, 2, false>(a, p.ps, p.h_kv, b.num_seqs, s);
+      return fp8 ? launch<128, 64, true>(a, p.ps, p.h_kv, b.num_seqs, s)
+                 : launch<128, 64, false>(a, p.ps, p.h_kv, b.num_seqs, s);
     case 256:
-      return fp8 ? launch<256, 32, 2, true>(a, p.ps, p.h_kv, b.num_seqs, s)
-                 : launch<256, 32, 2, false>(a, p.ps, p.h_kv, b.num_seqs, s);
+      return fp8 ? launch<256, 32, true>(a, p.ps, p.h_kv, b.num_seqs, s)
+                 : launch<256, 32, false>(a, p.ps, p.h_kv, b.num_seqs, s);
   }
   return hipErrorInvalidValue;
 }
