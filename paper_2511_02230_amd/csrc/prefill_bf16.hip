@@ -222,15 +222,15 @@ struct Tile {
   int g, t, ipos, i_min, i_max, kv_end, kb_begin, nblk, half, col, gq, li;
 };
 
-// Part P (0 or 1) of S^T = K Q^T for one block: the first or second half of
-// its NT x DS MFMAs, so that each half can be scheduled against a different
-// stretch of the previous block's softmax.  Row m of tile tt is key
-// 32 tt + pi(m).
+// Part P (0 or 1) of S^T = K Q^T for one block: k-steps [P DS/2, (P+1) DS/2)
+// of every tile, so that each half can be scheduled against a different
+// stretch of the previous block's softmax and holds NT independent
+// accumulation chains.  Row m of tile tt is key 32 tt + pi(m).
 template <class C, int P>
 __device__ __forceinline__ void qk_part(const lds_u8 *kb, const Tile<C> &T, f32x16 (&s)[C::NT]) {
 #pragma unroll
-  for (int n = P * C::NQK / 2; n < (P + 1) * C::NQK / 2; ++n) {
-    const int tt = n / C::DS, ds = n % C::DS;
+  for (int n = 0; n < C::NQK / 2; ++n) {
+    const int tt = n % C::NT, ds = P * (C::DS / 2) + n / C::NT;
     if (ds == 0) s[tt] = f32x16{};
     const int key = 32 * tt + pi_row(T.col);
     const int sw = swz_k<C::CH>(key);
@@ -239,19 +239,14 @@ __device__ __forceinline__ void qk_part(const lds_u8 *kb, const Tile<C> &T, f32x
   }
 }
 
-// Softmax of block j (scores s, raw K Q^T) and O^T += V^T P^T with V of
-// block j (bf16 layout at vb).  qk_part<1> of the next block is issued in
-// the middle, between the row maximum and the exponentials.
+// fp8 key scales and the causal / window mask of block j's scores (the
+// mask only on blocks that straddle the diagonal or the window edge).
 template <class C, int PS, bool FP8>
-__device__ __forceinline__ void softmax_pv(const PrefillArgs &a, const int32_t *bt, Tile<C> &T, int j,
-                                           f32x16 (&s)[C::NT], const lds_u8 *vb, const lds_u8 *kb_next,
-                                           f32x16 (&s_next)[C::NT]) {
+__device__ __forceinline__ void scale_mask(const PrefillArgs &a, const int32_t *bt, const Tile<C> &T,
+                                           int j, f32x16 (&s)[C::NT], float (&vsc)[C::NT * 2]) {
   constexpr int BN = C::BN_;
   const int kbase = (T.kb_begin + j) * BN;
   const int half = T.half;
-
-  // ---- fp8 key scales, mask, row maximum (in log2 units)
-  float vsc[C::NT * 2];  // fp8: V scale per 16-key group
   if constexpr (FP8) {
 #pragma unroll
     for (int q = 0; q < C::NT * 2; ++q) {
@@ -277,6 +272,16 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, const int32_t *
       }
     }
   }
+}
+
+// Softmax of block j (scores s after scale_mask) and O^T += V^T P^T with V
+// of block j (bf16 layout at vb).  The two halves of the next block's S^T
+// are issued around the row maximum, and before the exponentials.
+template <class C, int PS, bool FP8>
+__device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32x16 (&s)[C::NT],
+                                           const float (&vsc)[C::NT * 2], const lds_u8 *vb,
+                                           const lds_u8 *kb_next, f32x16 (&s_next)[C::NT]) {
+  qk_part<C, 0>(kb_next, T, s_next);
   float mx = kNegInf;
 #pragma unroll
   for (int tt = 0; tt < C::NT; ++tt)
@@ -390,9 +395,10 @@ __device__ __forceinline__ void step(const PrefillArgs &a, const int32_t *bt, Ti
     kb = R.k16;
     vb = R.v16;
   }
+  float vsc[C::NT * 2];
+  scale_mask<C, PS, FP8>(a, bt, T, j, s_cur, vsc);
   // (past the last block this reads a stale K stage; the result is unused)
-  qk_part<C, 0>(kb, T, s_nxt);
-  softmax_pv<C, PS, FP8>(a, bt, T, j, s_cur, vb, kb, s_nxt);
+  softmax_pv<C, PS, FP8>(a, T, s_cur, vsc, vb, kb, s_nxt);
 }
 
 template <int D, int BN, bool FP8, int PS>
