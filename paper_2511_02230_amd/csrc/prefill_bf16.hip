@@ -281,6 +281,7 @@ template <class C, int PS, bool FP8>
 __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32x16 (&s)[C::NT],
                                            const float (&vsc)[C::NT * 2], const lds_u8 *vb,
                                            const lds_u8 *kb_next, f32x16 (&s_next)[C::NT]) {
+  __builtin_amdgcn_s_setprio(1);
   qk_part<C, 0>(kb_next, T, s_next);
   float mx = kNegInf;
 #pragma unroll
@@ -350,6 +351,7 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32
       }
     }
   }
+  __builtin_amdgcn_s_setprio(0);
 }
 
 // The K ring holds K of blocks j+1 and j+2 while step j runs, the V ring V
