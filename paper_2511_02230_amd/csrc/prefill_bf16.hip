@@ -420,7 +420,28 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   // tiles streaming the same K/V share that XCD's L2
   const int g = blockIdx.x;
   const int tile = a.tiles - 1 - (int)blockIdx.y;  // later (costlier) tiles first
-  const int b = blockIdx.z;
+  // grid.z is a rank: sequences in decreasing per-tile cost (retained prefix
+  // plus new turn), so the longest tiles are dealt out first and the short
+  // ones fill the tail
+  __shared__ int rank_cost[kThreads];
+  __shared__ int rank_seq;
+  int b = blockIdx.z;
+  if ((int)gridDim.z <= kThreads) {
+    const int nb = gridDim.z, tid = threadIdx.x;
+    if (tid < nb) rank_cost[tid] = a.ctx[tid] + (a.cu[tid + 1] - a.cu[tid]);
+    __syncthreads();
+    if (tid < nb) {
+      const int c = rank_cost[tid];
+      int r = 0;
+      for (int o = 0; o < nb; ++o) {
+        const int co = rank_cost[o];
+        r += (co > c) | ((co == c) & (o < tid));
+      }
+      if (r == (int)blockIdx.z) rank_seq = tid;
+    }
+    __syncthreads();
+    b = __builtin_amdgcn_readfirstlane(rank_seq);
+  }
   const int q0 = a.cu[b];
   const int n = a.cu[b + 1] - q0;
   const int G = a.group;
