@@ -461,6 +461,18 @@ hipError_t launch_decode_bf16(const PoolView &p, const BatchView &b, const void 
   a.split_len = decode_split_len(p, b, h_q, split_len);
   a.max_splits = (int)((b.max_ctx + a.split_len - 1) / a.split_len);
   if (a.max_splits < 1) a.max_splits = 1;
+  if (split_len == 0 && window > 0 && window < b.max_ctx) {
+    // a sliding window sees at most `window` keys: size the partitions for
+    // that, as long as the partials still fit the workspace sized above
+    BatchView bw = b;
+    bw.max_ctx = window;
+    const int lw = decode_split_len(p, bw, h_q, 0);
+    const int sw = (window + lw - 1) / lw;
+    if (sw <= a.max_splits) {
+      a.split_len = lw;
+      a.max_splits = sw;
+    }
+  }
   a.head_chunks = (a.group + 15) / 16;
   float *w = static_cast<float *>(ws);
   const size_t n_o = (size_t)b.num_seqs * h_q * a.max_splits * p.d;
