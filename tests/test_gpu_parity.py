@@ -147,6 +147,11 @@ SMALL = [
     # rows whose window starts within the first keys of a block, while other
     # rows of the same wave already see keys in earlier blocks
     (cfg_of("w4", 16, 8, 128, 16, "bf16"), [(100, 60), (97, 70)], [130], 40),
+    # head_dim 256 on 64-token pages; a sequence with no new-turn rows in the
+    # prefill batch
+    (cfg_of("e1", 8, 2, 256, 64, "bf16"), [(100, 0), (64, 33), (0, 5)], [1, 130], 0),
+    (cfg_of("e2", 8, 2, 256, 64, "bf16"), [(200, 70)], [333], 50),
+    (cfg_of("e3", 16, 8, 64, 64, "fp8"), [(0, 40), (130, 0), (70, 17)], [1, 64, 129], 0),
     (cfg_of("f1", 4, 2, 64, 16, "f32", "f32"), [(30, 20), (0, 3)], [19, 50], 0),
     (cfg_of("f2", 4, 1, 128, 64, "f32", "f32"), [(70, 9)], [129], 5),
 ]
