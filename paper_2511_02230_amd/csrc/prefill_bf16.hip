@@ -80,7 +80,8 @@ struct Cfg {
   static constexpr int LDS = 4 * RAW_BLK + (FP8 ? 2 * BLK : 0);
   static_assert(RAW_BLK % 2048 == 0, "each wave issues whole 1-KB loads");
   static_assert(PS % RPD == 0, "a load never straddles a page");
-  static_assert(LDS <= 80 * 1024, "two workgroups per CU");
+  // two workgroups per CU below head_dim 256; one (as the registers allow) above
+  static_assert(LDS <= (D >= 256 ? 160 : 80) * 1024, "LDS budget");
 };
 
 // XOR swizzles of the 16-byte chunk index within a bf16 row.
@@ -576,7 +577,7 @@ hipError_t launch_prefill_bf16(const PoolView &p, const BatchView &b, const void
                  : launch<128, 64, false>(a, p.ps, p.h_kv, b.num_seqs, s);
     case 256:
       return fp8 ? launch<256, 32, true>(a, p.ps, p.h_kv, b.num_seqs, s)
-                 : launch<256, 32, false>(a, p.ps, p.h_kv, b.num_seqs, s);
+                 : launch<256, 64, false>(a, p.ps, p.h_kv, b.num_seqs, s);
   }
   return hipErrorInvalidValue;
 }
