@@ -110,16 +110,19 @@ ckv_status_t kv_append(const ckv_pool_t *pool, const ckv_batch_t *batch, const v
   return launched(ckv::launch_kv_append(view(pool), view(batch), k_new, v_new, in_dtype, stream));
 }
 
-size_t prefix_prefill_workspace_bytes(const ckv_pool_t *, const ckv_batch_t *, int32_t) {
-  return 0;
+size_t prefix_prefill_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t *batch,
+                                      int32_t num_q_heads) {
+  if (check_pool(pool) != CKV_OK || check_batch(pool, batch, 0) != CKV_OK ||
+      check_heads(pool, num_q_heads) != CKV_OK)
+    return 0;
+  if (batch->num_seqs == 0 || batch->total_q_len == 0 || pool->kv_dtype == CKV_F32) return 0;
+  return ckv::prefill_workspace_bytes(view(pool), view(batch), num_q_heads);
 }
 
 ckv_status_t prefix_prefill_attn(const ckv_pool_t *pool, const ckv_batch_t *batch, const void *q,
                                  ckv_dtype_t q_dtype, int32_t num_q_heads, float softmax_scale,
                                  int32_t window, void *out, void *workspace,
                                  size_t workspace_bytes, hipStream_t stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   CKV_TRY(check_pool(pool));
   CKV_TRY(check_batch(pool, batch, 0));
   CKV_TRY(check_heads(pool, num_q_heads));
@@ -131,8 +134,10 @@ ckv_status_t prefix_prefill_attn(const ckv_pool_t *pool, const ckv_batch_t *batc
     return launched(ckv::launch_attn_f32(view(pool), view(batch), static_cast<const float *>(q),
                                          num_q_heads, softmax_scale, window, false,
                                          static_cast<float *>(out), stream));
+  const size_t need = ckv::prefill_workspace_bytes(view(pool), view(batch), num_q_heads);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return CKV_ERR_WORKSPACE;
   return launched(ckv::launch_prefill_bf16(view(pool), view(batch), q, num_q_heads, softmax_scale,
-                                           window, out, stream));
+                                           window, out, workspace, stream));
 }
 
 size_t paged_decode_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t *batch,

@@ -26,8 +26,9 @@ hipError_t launch_kv_append(const PoolView &p, const BatchView &b, const void *k
 hipError_t launch_attn_f32(const PoolView &p, const BatchView &b, const float *q, int h_q,
                            float scale, int window, bool decode, float *out, hipStream_t s);
 
+size_t prefill_workspace_bytes(const PoolView &p, const BatchView &b, int h_q);
 hipError_t launch_prefill_bf16(const PoolView &p, const BatchView &b, const void *q, int h_q,
-                               float scale, int window, void *out, hipStream_t s);
+                               float scale, int window, void *out, void *ws, hipStream_t s);
 
 size_t decode_workspace_bytes(const PoolView &p, const BatchView &b, int h_q, int split_len);
 int decode_split_len(const PoolView &p, const BatchView &b, int h_q, int requested);

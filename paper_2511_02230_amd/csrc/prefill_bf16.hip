@@ -29,6 +29,8 @@
 //     only moves (and O is rescaled) when it grows by more than 2^8, which
 //     leaves the result unchanged but skips most rescales.  Masking only on
 //     blocks that straddle the causal diagonal or the window edge.
+#include <algorithm>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -44,7 +46,11 @@ struct PrefillArgs {
   int32_t max_pages, h_q, h_kv, group;
   float scale_log2;  // softmax_scale * log2(e)
   int32_t window;
-  int32_t tiles;     // grid.x: max row tiles of a sequence
+  int32_t tiles;      // grid.y: max row tiles of a sequence
+  int32_t splits;     // key partitions per row tile (grid.x = H_kv * splits)
+  int32_t split_len;  // keys per partition (a multiple of the block size)
+  float *part_o;      // splits > 1: [total_q * H_q][splits][D] fp32
+  float *part_ml;     // splits > 1: [total_q * H_q][splits][2] (m, l)
 };
 
 constexpr int kRows = 128;  // rows per workgroup
@@ -419,7 +425,10 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   // linear order, so with 8 KV heads every row tile of one (sequence, KV
   // head) lands on the same XCD, next to its neighbours in time, and the
   // tiles streaming the same K/V share that XCD's L2
-  const int g = blockIdx.x;
+  // grid.x = H_kv * splits with the KV head fastest, so the XCD grouping
+  // holds; with splits > 1 each workgroup covers one key partition
+  const int g = (int)blockIdx.x % a.h_kv;
+  const int split = (int)blockIdx.x / a.h_kv;
   const int tile = a.tiles - 1 - (int)blockIdx.y;  // later (costlier) tiles first
   // grid.z is a rank: sequences in decreasing per-tile cost (retained prefix
   // plus new turn), so the longest tiles are dealt out first and the short
@@ -477,9 +486,21 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   T.kv_end = T.i_max + 1;
   const int W = a.window;
   const int kv_begin = W > 0 ? max(0, T.i_min - W + 1) : 0;
-  T.kb_begin = kv_begin / BN;
-  const int kb_end = (T.kv_end + BN - 1) / BN;
+  // this workgroup's keys: the tile's visible range, cut to its partition
+  // (partitions are whole blocks, so every key lands in exactly one)
+  const int part_lo = split * a.split_len, part_hi = part_lo + a.split_len;
+  T.kb_begin = max(kv_begin, part_lo) / BN;
+  const int kb_end = (min(T.kv_end, part_hi) + BN - 1) / BN;
   T.nblk = kb_end - T.kb_begin;
+  const size_t prow = (size_t)(q0 + t) * a.h_q + (size_t)g * G + hh;  // (token, head) row
+  if (T.nblk <= 0) {
+    // an empty partition: weight 0 in the merge
+    if (rvalid && T.half == 0) {
+      const size_t pi = prow * a.splits + split;
+      st<f32x2>(a.part_ml + pi * 2, f32x2{kNegInf, 0.f});
+    }
+    return;
+  }
 
   lane_offsets<C, PS, FP8>(T.loff);
   // prologue: K of block 0, then K of block 1 and V of block 0 while S^T of
@@ -520,6 +541,21 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   // ---- normalize and store this lane's row: d = 32 dt + 8 i + 4 half + 0..3
   const float l = half_swap_sum(T.l);
   if (!rvalid) return;
+  if (a.splits > 1) {
+    // partial of this partition: (m, l) and o / l, merged by combine_kernel
+    const size_t pi = prow * a.splits + split;
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    float *po = a.part_o + pi * D;
+#pragma unroll
+    for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        st<f32x4>(po + 32 * dt + 8 * i + 4 * T.half,
+                  f32x4{T.o[dt][4 * i] * inv, T.o[dt][4 * i + 1] * inv, T.o[dt][4 * i + 2] * inv,
+                        T.o[dt][4 * i + 3] * inv});
+    if (T.half == 0) st<f32x2>(a.part_ml + pi * 2, f32x2{T.m, l});
+    return;
+  }
   const float inv = 1.f / l;
   uint16_t *orow = a.out + qrow;
 #pragma unroll
@@ -533,20 +569,88 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   }
 }
 
+// Merge the key partitions of one (token, head) row:
+// w_s = l_s 2^(m_s - M), out = sum_s w_s o_s / sum_s w_s  (m in log2 units).
+template <int D>
+__global__ __launch_bounds__(64) void combine_kernel(PrefillArgs a) {
+  const size_t row = blockIdx.x;
+  const size_t base = row * a.splits;
+  float M = kNegInf;
+  for (int s = 0; s < a.splits; ++s) M = fmaxf(M, a.part_ml[(base + s) * 2]);
+  float acc[D / 64];
+#pragma unroll
+  for (int k = 0; k < D / 64; ++k) acc[k] = 0.f;
+  float wsum = 0.f;
+  for (int s = 0; s < a.splits; ++s) {
+    const float ms = a.part_ml[(base + s) * 2];
+    const float ls = a.part_ml[(base + s) * 2 + 1];
+    const float w = ms == kNegInf ? 0.f : ls * fast_exp2(ms - M);
+    wsum += w;
+    if (w == 0.f) continue;  // empty partition: its o was never written
+    const float *po = a.part_o + (base + s) * D;
+#pragma unroll
+    for (int k = 0; k < D / 64; ++k) acc[k] = fmaf(w, po[threadIdx.x + 64 * k], acc[k]);
+  }
+  const float inv = 1.f / wsum;
+  uint16_t *orow = a.out + row * D;
+#pragma unroll
+  for (int k = 0; k < D / 64; ++k) {
+    const uint32_t pk = pack_bf16x2(acc[k] * inv, 0.f);
+    orow[threadIdx.x + 64 * k] = (uint16_t)(pk & 0xffffu);
+  }
+}
+
 template <int D, int BN, bool FP8>
-hipError_t launch(const PrefillArgs &a, int ps, int h_kv, int num_seqs, hipStream_t s) {
-  dim3 grid(h_kv, a.tiles, num_seqs);
+hipError_t launch(const PrefillArgs &a, int ps, int h_kv, int num_seqs, int total_q, hipStream_t s) {
+  dim3 grid(h_kv * a.splits, a.tiles, num_seqs);
   if (ps == 16)
     hipLaunchKernelGGL((prefill_kernel<D, BN, FP8, 16>), grid, dim3(kThreads), 0, s, a);
   else
     hipLaunchKernelGGL((prefill_kernel<D, BN, FP8, 64>), grid, dim3(kThreads), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.splits <= 1) return e;
+  hipLaunchKernelGGL((combine_kernel<D>), dim3((unsigned)total_q * a.h_q), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 
+// Keys per block of the kernel instantiated for (D, fp8).
+int prefill_block_keys(int d, bool fp8) { return d >= 256 && fp8 ? 32 : 64; }
+
 }  // namespace
 
+// Key partitions per row tile: one while the row tiles alone fill the GPU
+// (twice the resident workgroups); otherwise enough to fill it, with at
+// least 1024 keys per partition and at most 32 partitions.
+void prefill_splits(const PoolView &p, const BatchView &b, int h_q, int *splits, int *split_len) {
+  const int group = h_q / p.h_kv;
+  const long long tiles = ((long long)b.max_q * group + kRows - 1) / kRows;
+  const long long items = tiles * p.h_kv * b.num_seqs;
+  const long long slots = (p.d >= 256 ? 1 : 2) * 256;
+  const long long max_kv = (long long)b.max_ctx + b.max_q;
+  const int bn = prefill_block_keys(p.d, p.kv_dtype == 2);
+  long long s = 1;
+  if (items > 0 && items < 2 * slots) {
+    s = (2 * slots + items - 1) / items;
+    s = std::min<long long>(s, (max_kv + 1023) / 1024);
+    s = std::max<long long>(std::min<long long>(s, 32), 1);
+  }
+  long long len = (max_kv + s - 1) / s;
+  len = (len + bn - 1) / bn * bn;
+  if (len < bn) len = bn;
+  *split_len = (int)len;
+  *splits = (int)((max_kv + len - 1) / len);
+  if (*splits < 1) *splits = 1;
+}
+
+size_t prefill_workspace_bytes(const PoolView &p, const BatchView &b, int h_q) {
+  int splits, len;
+  prefill_splits(p, b, h_q, &splits, &len);
+  if (splits <= 1) return 0;
+  return (size_t)b.total_q * h_q * splits * (p.d + 2) * sizeof(float);
+}
+
 hipError_t launch_prefill_bf16(const PoolView &p, const BatchView &b, const void *q, int h_q,
-                               float scale, int window, void *out, hipStream_t s) {
+                               float scale, int window, void *out, void *ws, hipStream_t s) {
   if (b.num_seqs == 0 || b.max_q == 0 || b.total_q == 0) return hipSuccess;
   PrefillArgs a;
   a.q = static_cast<const uint16_t *>(q);
@@ -567,17 +671,22 @@ hipError_t launch_prefill_bf16(const PoolView &p, const BatchView &b, const void
   const long long rows = (long long)b.max_q * a.group;
   a.tiles = (int)((rows + kRows - 1) / kRows);
   if (a.tiles > 65535) return hipErrorInvalidConfiguration;  // grid.y limit
+  prefill_splits(p, b, h_q, &a.splits, &a.split_len);
+  float *w = static_cast<float *>(ws);
+  a.part_o = a.splits > 1 ? w : nullptr;
+  a.part_ml = a.splits > 1 ? w + (size_t)b.total_q * h_q * a.splits * p.d : nullptr;
   const bool fp8 = p.kv_dtype == 2;
+  const int tq = b.total_q;
   switch (p.d) {
     case 64:
-      return fp8 ? launch<64, 64, true>(a, p.ps, p.h_kv, b.num_seqs, s)
-                 : launch<64, 64, false>(a, p.ps, p.h_kv, b.num_seqs, s);
+      return fp8 ? launch<64, 64, true>(a, p.ps, p.h_kv, b.num_seqs, tq, s)
+                 : launch<64, 64, false>(a, p.ps, p.h_kv, b.num_seqs, tq, s);
     case 128:
-      return fp8 ? launch<128, 64, true>(a, p.ps, p.h_kv, b.num_seqs, s)
-                 : launch<128, 64, false>(a, p.ps, p.h_kv, b.num_seqs, s);
+      return fp8 ? launch<128, 64, true>(a, p.ps, p.h_kv, b.num_seqs, tq, s)
+                 : launch<128, 64, false>(a, p.ps, p.h_kv, b.num_seqs, tq, s);
     case 256:
-      return fp8 ? launch<256, 32, true>(a, p.ps, p.h_kv, b.num_seqs, s)
-                 : launch<256, 64, false>(a, p.ps, p.h_kv, b.num_seqs, s);
+      return fp8 ? launch<256, 32, true>(a, p.ps, p.h_kv, b.num_seqs, tq, s)
+                 : launch<256, 64, false>(a, p.ps, p.h_kv, b.num_seqs, tq, s);
   }
   return hipErrorInvalidValue;
 }

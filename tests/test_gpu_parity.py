@@ -152,6 +152,11 @@ SMALL = [
     (cfg_of("e1", 8, 2, 256, 64, "bf16"), [(100, 0), (64, 33), (0, 5)], [1, 130], 0),
     (cfg_of("e2", 8, 2, 256, 64, "bf16"), [(200, 70)], [333], 50),
     (cfg_of("e3", 16, 8, 64, 64, "fp8"), [(0, 40), (130, 0), (70, 17)], [1, 64, 129], 0),
+    # few row tiles over long prefixes: the prefill splits each tile's keys
+    # into partitions and merges them
+    (cfg_of("s1", 32, 8, 128, 16, "bf16"), [(6000, 300)], [6300], 0),
+    (cfg_of("s2", 16, 8, 256, 16, "bf16"), [(5000, 100)], [5100], 700),
+    (cfg_of("s3", 24, 2, 128, 64, "fp8"), [(4000, 64), (100, 20)], [4064], 0),
     (cfg_of("f1", 4, 2, 64, 16, "f32", "f32"), [(30, 20), (0, 3)], [19, 50], 0),
     (cfg_of("f2", 4, 1, 128, 64, "f32", "f32"), [(70, 9)], [129], 5),
 ]
