@@ -129,7 +129,12 @@ ckv_status_t kv_append(const ckv_pool_t *pool, const ckv_batch_t *batch,
  * K_j, V_j being KV head h / G of position j read through the block table.
  *   q, out: [total_q_len][num_q_heads][head_dim]; out has q_dtype.
  *   Softmax and accumulation are fp32; BF16 products run on MFMA in bf16.
- *   workspace: at least prefix_prefill_workspace_bytes(...) bytes (may be 0).
+ *   workspace: at least prefix_prefill_workspace_bytes(...) bytes, device
+ *   memory owned by the caller and free for the duration of the call.  It is
+ *   0 when the batch's row tiles fill the GPU; otherwise each tile's keys are
+ *   split into partitions whose fp32 partials land there before a merge
+ *   (total_q_len * num_q_heads * partitions * (head_dim + 2) * 4 bytes).
+ *   Too small a workspace returns CKV_ERR_WORKSPACE and launches nothing.
  */
 ckv_status_t prefix_prefill_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
                                  const void *q, ckv_dtype_t q_dtype, int32_t num_q_heads,
