@@ -1,7 +1,8 @@
 /*
  * ckv.h -- paged KV-cache hot path for multi-turn agent serving on MI355X
  * (gfx950): append new-turn K/V into a paged pool, prefix-reuse prefill
- * attention, paged decode attention.
+ * attention, paged decode attention, and whole-page moves between the pool
+ * and host memory (offload on eviction, reload on a TTL miss).
  *
  * Why this path exists: Continuum (arXiv 2511.02230) keeps a tool-calling
  * request's KV blocks resident in GPU memory for a time-to-live instead of
@@ -18,9 +19,10 @@
  * --------------------------------
  *  - Every pointer argument is a HIP device pointer owned by the caller,
  *    except the ckv_pool_t / ckv_batch_t structs themselves (host memory,
- *    read during the call only).  The library keeps no state, never
- *    allocates or frees memory and never synchronizes; all work is enqueued
- *    on `stream` (0 = the null stream).  Calls are re-entrant.
+ *    read during the call only) and the host_* buffers of kv_pages_reload /
+ *    kv_pages_offload.  The library keeps no state, never allocates or frees
+ *    memory and never synchronizes; all work is enqueued on `stream` (0 = the
+ *    null stream).  Calls are re-entrant.
  *  - Pool layout: K and V are each [num_pages][num_kv_heads][page_size]
  *    [head_dim], row-major, element type kv_dtype.  For CKV_FP8_E4M3 each
  *    (page, kv head) has an fp32 scale in k_scale / v_scale
@@ -164,6 +166,59 @@ size_t prefix_prefill_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t 
                                       int32_t num_q_heads);
 size_t paged_decode_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t *batch,
                                     int32_t num_q_heads, int32_t kv_split_len);
+
+/*
+ * kv_pages_offload / kv_pages_reload -- copy whole pool pages to host memory
+ * and back, bit for bit: K and V pages and, for FP8_E4M3 pools, their
+ * per-(page, head) scales.  With CPU offloading on, an evicted request's KV
+ * cache goes to host memory and a later turn that finds it gone reloads it
+ * instead of re-running prefill (Sec. 1; Sec. 3.2); the time this takes is
+ * one of the two readings of Prefill-Reload(r) in the cost model (Sec. 4.1),
+ * and the host-link throughput it runs at is the first quantity of the
+ * offline profile (Sec. 5.2, "Offline Profile", item (1)).
+ *   pages: DEVICE int32 [num_moved], pool page ids; host page i corresponds to
+ *     pool page pages[i] (e.g. the first ceil(c / page_size) entries of a
+ *     sequence's block-table row).  Ids outside [0, num_pages) are skipped:
+ *     the pool is never touched outside its pages, and offload leaves that
+ *     host page's contents unspecified.  Reload ids must be distinct (a
+ *     repeated id leaves that pool page's contents unspecified).
+ *   host_k, host_v: HOST memory, [num_moved][num_kv_heads][page_size]
+ *     [head_dim] in kv_dtype, dense.  host_k_scale, host_v_scale: HOST fp32
+ *     [num_moved][num_kv_heads], FP8_E4M3 pools only (may be NULL otherwise).
+ *     Memory from hipHostMalloc (pinned) is copied asynchronously at host-link
+ *     rate; pageable memory is accepted, but HIP then copies through its own
+ *     bounce buffers and the call may block the calling thread.
+ *   staging: device memory, 16-byte aligned, at least
+ *     kv_pages_staging_bytes(pool, num_moved) bytes (the moved pages, dense),
+ *     owned by the caller and free until the stream has passed the call.
+ * Reload: host -> staging by hipMemcpyAsync, then a kernel scatters staging
+ * page i into pool page pages[i].  Offload: a kernel gathers pool page
+ * pages[i] into staging page i, then hipMemcpyAsync copies staging -> host.
+ * Staging holds K pages, V pages, K scales, V scales back to back; host
+ * buffers that are adjacent in that same order (host_v == host_k + K bytes,
+ * and so on) move as one copy, which saves a copy's fixed cost on small
+ * moves.
+ * Pool pages not named in `pages` are untouched.  The host buffers may be
+ * reused (reload) or read (offload) once the stream has passed the call.
+ * Errors: CKV_ERR_INVALID_ARG for a NULL or unaligned pointer, num_moved < 0
+ * or a move too large for one launch; CKV_ERR_WORKSPACE for a missing or
+ * small staging buffer; CKV_ERR_LAUNCH when a copy or the kernel fails to
+ * enqueue.  num_moved == 0 does nothing.
+ */
+ckv_status_t kv_pages_reload(const ckv_pool_t *pool, const int32_t *pages, int32_t num_moved,
+                             const void *host_k, const void *host_v,
+                             const float *host_k_scale, const float *host_v_scale,
+                             void *staging, size_t staging_bytes, hipStream_t stream);
+ckv_status_t kv_pages_offload(const ckv_pool_t *pool, const int32_t *pages, int32_t num_moved,
+                              void *host_k, void *host_v, float *host_k_scale,
+                              float *host_v_scale, void *staging, size_t staging_bytes,
+                              hipStream_t stream);
+
+/* Staging bytes for moving num_moved pages of `pool`:
+ * 2 * num_moved * num_kv_heads * page_size * head_dim * sizeof(kv_dtype),
+ * plus 2 * num_moved * num_kv_heads * 4 for FP8_E4M3.  0 for invalid
+ * arguments or num_moved <= 0. */
+size_t kv_pages_staging_bytes(const ckv_pool_t *pool, int32_t num_moved);
 
 /*
  * ckv_validate_batch -- host-side check of the device-side contract, on HOST

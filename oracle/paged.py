@@ -15,6 +15,10 @@ Profile"):
            sequence with j <= i (and i - j < W for a window W > 0), read
            through the block table; query head h uses KV head h // G.
   decode   the same for one query at position c_b - 1 over c_b tokens.
+  offload / reload
+           whole pages copied to host memory and back, bit for bit, when
+           CPU offloading is on (an evicted request's cache returns without
+           a new prefill, Sec. 1 and Sec. 3.2).
 
 The pool is [num_pages, H_kv, page_size, D] for K and for V, stored as
 float32, bfloat16 bit patterns (uint16) or E4M3FN codes (uint8) with one
@@ -232,3 +236,36 @@ def lse_merge(parts):
     M = ms.max(axis=0)
     w = np.where(np.isfinite(ms), ls * np.exp(ms - M), 0.0)
     return (w[:, :, None] * os_).sum(axis=0) / w.sum(axis=0)[:, None]
+
+
+# ------------------------------------------------------- page offload/reload
+
+def offload_pages(pool, pages, scale=None):
+    """Host copy of pool pages: host page i is pool page pages[i], byte for
+    byte, with its (page, head) scales for fp8.  An evicted request's pages
+    leave the GPU this way when CPU offloading is on (Sec. 1; Sec. 3.2).
+    Ids outside [0, num_pages) give an all-zero host page here; the library
+    leaves such a page unspecified, so tests compare valid ids only."""
+    num_pages = pool.shape[0]
+    host = np.zeros((len(pages),) + pool.shape[1:], dtype=pool.dtype)
+    host_scale = None if scale is None else np.zeros((len(pages), pool.shape[1]), dtype=scale.dtype)
+    for i, p in enumerate(pages):
+        if 0 <= p < num_pages:
+            host[i] = pool[p]
+            if scale is not None:
+                host_scale[i] = scale[p]
+    return host, host_scale
+
+
+def reload_pages(pool, pages, host, scale=None, host_scale=None):
+    """Write host page i into pool page pages[i] (in place), scales likewise:
+    a TTL miss with offloading on brings the pages back instead of
+    re-running prefill (Sec. 1; Sec. 3.2; Prefill-Reload(r), Sec. 4.1).
+    Ids outside [0, num_pages) are skipped; every other pool page keeps its
+    bytes."""
+    num_pages = pool.shape[0]
+    for i, p in enumerate(pages):
+        if 0 <= p < num_pages:
+            pool[p] = host[i]
+            if scale is not None:
+                scale[p] = host_scale[i]

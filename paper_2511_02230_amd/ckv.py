@@ -23,7 +23,8 @@ CKV_F32, CKV_BF16, CKV_FP8_E4M3 = 0, 1, 2
 STATUS = {0: "CKV_OK", 1: "CKV_ERR_INVALID_ARG", 2: "CKV_ERR_UNSUPPORTED", 3: "CKV_ERR_WORKSPACE",
           4: "CKV_ERR_LAUNCH"}
 EXPORTS = ("kv_append", "prefix_prefill_attn", "paged_decode_attn", "prefix_prefill_workspace_bytes",
-           "paged_decode_workspace_bytes", "ckv_validate_batch", "ckv_status_string", "ckv_version")
+           "paged_decode_workspace_bytes", "kv_pages_reload", "kv_pages_offload",
+           "kv_pages_staging_bytes", "ckv_validate_batch", "ckv_status_string", "ckv_version")
 
 
 class CkvError(RuntimeError):
@@ -59,6 +60,9 @@ def _load():
         "paged_decode_attn": ([P, B, vp, ctypes.c_int, i32, f32, i32, i32, vp, vp, sz, vp], ctypes.c_int),
         "prefix_prefill_workspace_bytes": ([P, B, i32], sz),
         "paged_decode_workspace_bytes": ([P, B, i32, i32], sz),
+        "kv_pages_reload": ([P, vp, i32, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "kv_pages_offload": ([P, vp, i32, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "kv_pages_staging_bytes": ([P, i32], sz),
         "ckv_validate_batch": ([P, i32, i32, vp, vp, vp, i32, i32, i32, i32], ctypes.c_int),
         "ckv_status_string": ([ctypes.c_int], ctypes.c_char_p),
         "ckv_version": ([], i32),
@@ -235,6 +239,81 @@ def paged_decode_attn(pool: Pool, batch: Batch, q: torch.Tensor, softmax_scale: 
         float(softmax_scale), int(window), int(kv_split_len), _ptr(out), _ptr(ws), wsb,
         _stream(stream)))
     return out
+
+
+def pages_staging_bytes(pool: Pool, num_moved: int) -> int:
+    pc = pool.c()
+    return int(LIB.kv_pages_staging_bytes(ctypes.byref(pc), int(num_moved)))
+
+
+def _host(t: torch.Tensor, name: str, dtype, shape):
+    if t.is_cuda:
+        raise ValueError(f"{name} must be a host tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must be {dtype} {tuple(shape)}, got {t.dtype} {tuple(t.shape)}")
+
+
+def _page_move_args(pool: Pool, pages: torch.Tensor, host, staging):
+    _dev(pages, "pages", torch.int32)
+    if pages.dim() != 1:
+        raise ValueError("pages must be 1-D")
+    n = int(pages.shape[0])
+    page_shape = (n,) + tuple(pool.k.shape[1:])
+    fp8 = pool.kv_dtype == CKV_FP8_E4M3
+    names = ("host_k", "host_v", "host_k_scale", "host_v_scale")
+    for i, t in enumerate(host):
+        if i < 2:
+            _host(t, names[i], pool.k.dtype, page_shape)
+        elif fp8:
+            _host(t, names[i], torch.float32, page_shape[:2])
+    staging, sb = _workspace(pages_staging_bytes(pool, n), staging, pool.k.device)
+    ptrs = [_ptr(t) for t in host[:2]] + [_ptr(t) if fp8 else None for t in host[2:]]
+    return n, ptrs, staging, sb
+
+
+def kv_pages_reload(pool: Pool, pages: torch.Tensor, host_k: torch.Tensor, host_v: torch.Tensor,
+                    host_k_scale: Optional[torch.Tensor] = None,
+                    host_v_scale: Optional[torch.Tensor] = None, staging=None, stream=None):
+    """Copy host pages i (host_k / host_v [n, H_kv, page_size, D] in the pool's
+    dtype, pinned for an asynchronous copy; fp8 scales [n, H_kv]) into pool
+    pages pages[i] (int32 on the GPU).  Enqueued on the stream only."""
+    host = (host_k, host_v, host_k_scale, host_v_scale)
+    n, ptrs, st, sb = _page_move_args(pool, pages, host, staging)
+    pc = pool.c()
+    _check("kv_pages_reload", LIB.kv_pages_reload(ctypes.byref(pc), _ptr(pages), n, *ptrs, _ptr(st), sb,
+                                                  _stream(stream)))
+
+
+def kv_pages_offload(pool: Pool, pages: torch.Tensor, host_k=None, host_v=None, host_k_scale=None,
+                     host_v_scale=None, staging=None, stream=None):
+    """Copy pool pages pages[i] into host pages i.  Missing host buffers come
+    from one pinned allocation laid out like the staging area (K pages, V
+    pages, then fp8 scales), so the host side moves as a single copy.
+    Returns (host_k, host_v, host_k_scale, host_v_scale); they hold the pages
+    once the stream has passed the call."""
+    n = int(pages.shape[0])
+    shape = (n,) + tuple(pool.k.shape[1:])
+    if host_k is None or host_v is None:
+        fp8 = pool.kv_dtype == CKV_FP8_E4M3
+        nb = n * pool.k[0].numel() * pool.k.element_size() if n else 0
+        sb = n * pool.k.shape[1] * 4 if fp8 else 0
+        buf = torch.empty(2 * nb + 2 * sb, dtype=torch.uint8, pin_memory=True)
+        host_k = buf[:nb].view(pool.k.dtype).view(shape)
+        host_v = buf[nb:2 * nb].view(pool.k.dtype).view(shape)
+        if fp8:
+            host_k_scale = buf[2 * nb:2 * nb + sb].view(torch.float32).view(shape[:2])
+            host_v_scale = buf[2 * nb + sb:].view(torch.float32).view(shape[:2])
+    elif pool.kv_dtype == CKV_FP8_E4M3 and (host_k_scale is None or host_v_scale is None):
+        host_k_scale = torch.empty(shape[:2], dtype=torch.float32, pin_memory=True)
+        host_v_scale = torch.empty(shape[:2], dtype=torch.float32, pin_memory=True)
+    host = (host_k, host_v, host_k_scale, host_v_scale)
+    n, ptrs, st, sb = _page_move_args(pool, pages, host, staging)
+    pc = pool.c()
+    _check("kv_pages_offload", LIB.kv_pages_offload(ctypes.byref(pc), _ptr(pages), n, *ptrs, _ptr(st), sb,
+                                                    _stream(stream)))
+    return host
 
 
 def validate_batch(num_pages: int, page_size: int, block_table: np.ndarray, ctx_lens: np.ndarray,

@@ -2,6 +2,7 @@
 // Declarations and the contract of every entry point are in include/ckv.h.
 #include "../../include/ckv.h"
 
+#include <climits>
 #include <cmath>
 #include <unordered_set>
 #include <vector>
@@ -92,6 +93,20 @@ ckv_status_t launched(hipError_t e) { return e == hipSuccess ? CKV_OK : CKV_ERR_
     if (st_ != CKV_OK) return st_;       \
   } while (0)
 
+ckv_status_t check_page_move(const ckv_pool_t *pool, const int32_t *pages, int32_t n,
+                             const void *host_k, const void *host_v, const void *host_ks,
+                             const void *host_vs, const void *staging, size_t staging_bytes) {
+  CKV_TRY(check_pool(pool));
+  if (n < 0) return CKV_ERR_INVALID_ARG;
+  if (n == 0) return CKV_OK;
+  if (!pages || !host_k || !host_v) return CKV_ERR_INVALID_ARG;
+  if (pool->kv_dtype == CKV_FP8_E4M3 && (!host_ks || !host_vs)) return CKV_ERR_INVALID_ARG;
+  if ((long long)n * ckv::page_blocks(view(pool)) > INT_MAX) return CKV_ERR_INVALID_ARG;
+  if (!staging || staging_bytes < ckv::pages_staging_bytes(view(pool), n)) return CKV_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(staging) % 16 != 0) return CKV_ERR_INVALID_ARG;
+  return CKV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -177,6 +192,33 @@ ckv_status_t paged_decode_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
                                           stream));
 }
 
+size_t kv_pages_staging_bytes(const ckv_pool_t *pool, int32_t num_moved) {
+  if (check_pool(pool) != CKV_OK || num_moved <= 0) return 0;
+  return ckv::pages_staging_bytes(view(pool), num_moved);
+}
+
+ckv_status_t kv_pages_reload(const ckv_pool_t *pool, const int32_t *pages, int32_t num_moved,
+                             const void *host_k, const void *host_v, const float *host_k_scale,
+                             const float *host_v_scale, void *staging, size_t staging_bytes,
+                             hipStream_t stream) {
+  CKV_TRY(check_page_move(pool, pages, num_moved, host_k, host_v, host_k_scale, host_v_scale,
+                          staging, staging_bytes));
+  if (num_moved == 0) return CKV_OK;
+  return launched(ckv::launch_pages_reload(view(pool), host_k, host_v, host_k_scale, host_v_scale,
+                                           pages, num_moved, staging, stream));
+}
+
+ckv_status_t kv_pages_offload(const ckv_pool_t *pool, const int32_t *pages, int32_t num_moved,
+                              void *host_k, void *host_v, float *host_k_scale,
+                              float *host_v_scale, void *staging, size_t staging_bytes,
+                              hipStream_t stream) {
+  CKV_TRY(check_page_move(pool, pages, num_moved, host_k, host_v, host_k_scale, host_v_scale,
+                          staging, staging_bytes));
+  if (num_moved == 0) return CKV_OK;
+  return launched(ckv::launch_pages_offload(view(pool), pages, num_moved, host_k, host_v,
+                                            host_k_scale, host_v_scale, staging, stream));
+}
+
 ckv_status_t ckv_validate_batch(const ckv_pool_t *pool, int32_t num_seqs, int32_t max_pages_per_seq,
                                 const int32_t *bt, const int32_t *ctx, const int32_t *cu,
                                 int32_t max_q_len, int32_t max_ctx_len, int32_t mode,
@@ -220,7 +262,7 @@ const char *ckv_status_string(ckv_status_t status) {
     case CKV_ERR_WORKSPACE:
       return "CKV_ERR_WORKSPACE: workspace missing or too small";
     case CKV_ERR_LAUNCH:
-      return "CKV_ERR_LAUNCH: kernel launch failed";
+      return "CKV_ERR_LAUNCH: kernel launch or copy failed";
   }
   return "unknown ckv status";
 }

@@ -37,4 +37,14 @@ hipError_t launch_decode_bf16(const PoolView &p, const BatchView &b, const void 
                               float scale, int window, int split_len, void *out, void *ws,
                               size_t ws_bytes, hipStream_t s);
 
+int page_bytes(const PoolView &p);
+int page_blocks(const PoolView &p);
+size_t pages_staging_bytes(const PoolView &p, int n);
+hipError_t launch_pages_reload(const PoolView &p, const void *host_k, const void *host_v,
+                               const float *host_ks, const float *host_vs, const int32_t *pages,
+                               int n, void *staging, hipStream_t s);
+hipError_t launch_pages_offload(const PoolView &p, const int32_t *pages, int n, void *host_k,
+                                void *host_v, float *host_ks, float *host_vs, void *staging,
+                                hipStream_t s);
+
 }  // namespace ckv

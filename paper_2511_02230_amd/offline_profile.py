@@ -1,10 +1,15 @@
-"""Offline prefill-vs-context profile on one MI355X (one attention layer).
+"""Offline profile on one MI355X (one attention layer): host-link page
+throughput and prefill time against context length.
 
 Continuum's cost model needs the time to rebuild a request's KV cache when
-its TTL has expired (Prefill-Reload(r), Sec. 4.1).  The paper gets it from a
-short offline profile per (hardware, model): prefill for a ladder of context
-sizes up to the maximum context, then a quadratic fit of time against
-context length (Sec. 5.2, "Offline Profile").  Serving engines prefill in
+its TTL has expired (Prefill-Reload(r), Sec. 4.1): a reload from host memory
+when CPU offloading is on, else a new prefill.  The paper gets both from a
+short offline profile per (hardware, model) (Sec. 5.2, "Offline Profile"):
+(1) the GPU-CPU throughput of offloading, and (2) prefill for a ladder of
+context sizes up to the maximum context, then a quadratic fit of time
+against context length.  (1) here times kv_pages_offload / kv_pages_reload
+on whole pages of the model's pool layout, beside a plain pinned-memory
+copy of the same bytes (the link's practical rate).  For (2), serving engines prefill in
 chunks (the paper's vLLM baseline uses 2048-token chunks, Sec. 6.1), so the
 profile here measures both
 
@@ -19,6 +24,7 @@ this library does not run.
 
     python -m paper_2511_02230_amd.offline_profile --config llama3.1-70b \
         --max-len 65536 --chunks 256 512 1024 2048 4096
+    python -m paper_2511_02230_amd.offline_profile --config llama3.1-70b --transfer
 
 One sequence of max-len tokens is appended to the pool once; every timed
 call is a view of it (block table, ctx_lens = P, cu_q_lens = [0, n]).
@@ -66,6 +72,22 @@ def fit_quadratic(lengths: Sequence[float], times: Sequence[float]) -> Dict[str,
     ss_tot = float(((y - y.mean()) ** 2).sum())
     r2 = 1.0 - float((resid ** 2).sum()) / ss_tot if ss_tot > 0 else 1.0
     return {"a": float(a), "b": float(b), "c": float(c), "r2": r2}
+
+
+def fit_linear(sizes: Sequence[float], times: Sequence[float]) -> Dict[str, float]:
+    """Least-squares t = t0 + x / bw for transfer sizes x (bytes) and times t
+    (ms): bw in GB/s, t0 in microseconds, and R^2 of the fit."""
+    x = np.asarray(sizes, dtype=np.float64)
+    y = np.asarray(times, dtype=np.float64)
+    if x.size < 2:
+        raise ValueError("a line needs at least two points")
+    A = np.stack([x, np.ones_like(x)], axis=1)
+    (slope, t0), *_ = np.linalg.lstsq(A, y, rcond=None)
+    resid = y - A @ np.array([slope, t0])
+    ss_tot = float(((y - y.mean()) ** 2).sum())
+    r2 = 1.0 - float((resid ** 2).sum()) / ss_tot if ss_tot > 0 else 1.0
+    return {"gbps": float(1e-6 / slope) if slope > 0 else float("inf"), "t0_us": float(t0 * 1e3),
+            "r2": r2}
 
 
 def attention_flops(P: int, n: int, num_q_heads: int, head_dim: int, window: int = 0) -> float:
@@ -126,6 +148,116 @@ class PrefillTimer:
         return float(np.median(times))
 
 
+class TransferTimer:
+    """Pool of the model's page layout, pinned host pages and staging for up
+    to max_pages pages; times offload and reload of n pages named by a
+    shuffled page list, and a plain pinned copy of the same bytes."""
+
+    def __init__(self, cfg, max_pages: int, pool_pages: int = 0, device="cuda", seed: int = 0):
+        import torch
+
+        from . import ckv
+
+        self.torch, self.ckv, self.cfg = torch, ckv, cfg
+        pool_pages = pool_pages or 4 * max_pages
+        dt = {"f32": torch.float32, "bf16": torch.bfloat16, "fp8": torch.uint8}[cfg.kv_dtype]
+        shape = (pool_pages, cfg.num_kv_heads, cfg.page_size, cfg.head_dim)
+        g = torch.Generator(device=device).manual_seed(seed)
+        k = torch.randint(0, 256, shape + (torch.finfo(dt).bits // 8 if dt.is_floating_point else 1,),
+                          dtype=torch.uint8, device=device, generator=g).view(dt).view(shape)
+        v = k.roll(1, 0).contiguous()
+        ks = vs = None
+        if cfg.kv_dtype == "fp8":
+            ks = torch.rand(shape[:2], device=device, generator=g) + 0.5
+            vs = ks.flip(0).contiguous()
+        self.pool = ckv.Pool(k, v, ks, vs)
+        self.pages = torch.randperm(pool_pages, device=device, generator=g)[:max_pages].to(torch.int32)
+        self.page_shape, self.dt = shape[1:], dt
+        self.host_buf = torch.empty(ckv.pages_staging_bytes(self.pool, max_pages), dtype=torch.uint8,
+                                    pin_memory=True)
+        self.staging = torch.empty(ckv.pages_staging_bytes(self.pool, max_pages), dtype=torch.uint8,
+                                   device=device)
+        self.dev_flat = torch.empty(2 * k[0].numel() * k.element_size() * max_pages, dtype=torch.uint8,
+                                    device=device)
+        self.host_flat = torch.empty(self.dev_flat.numel(), dtype=torch.uint8, pin_memory=True)
+        self.max_pages = max_pages
+
+    def host_views(self, n: int):
+        """K pages, V pages and fp8 scales of n pages, back to back in one
+        pinned buffer (the layout that moves as a single copy)."""
+        torch = self.torch
+        nb = n * int(np.prod(self.page_shape)) * self.pool.k.element_size()
+        sb = n * self.cfg.num_kv_heads * 4 if self.cfg.kv_dtype == "fp8" else 0
+        b = self.host_buf
+        hk = b[:nb].view(self.dt).view((n,) + self.page_shape)
+        hv = b[nb:2 * nb].view(self.dt).view((n,) + self.page_shape)
+        if not sb:
+            return hk, hv, None, None
+        return (hk, hv, b[2 * nb:2 * nb + sb].view(torch.float32).view(n, -1),
+                b[2 * nb + sb:2 * nb + 2 * sb].view(torch.float32).view(n, -1))
+
+    def page_bytes(self, n: int) -> int:
+        """K + V (+ fp8 scales) bytes of n pages."""
+        b = 2 * n * self.pool.k[0].numel() * self.pool.k.element_size()
+        if self.cfg.kv_dtype == "fp8":
+            b += 2 * n * self.cfg.num_kv_heads * 4
+        return b
+
+    def _time(self, fn, reps: int, warmup: int) -> float:
+        torch = self.torch
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        return float(np.median(times))
+
+    def time(self, n: int, reps: int = 5, warmup: int = 2) -> Dict[str, float]:
+        """Milliseconds for offload, reload and a plain copy each way of n pages."""
+        if not 0 < n <= self.max_pages:
+            raise ValueError("n must lie in [1, max_pages]")
+        ckv, pg = self.ckv, self.pages[:n]
+        hk, hv, hks, hvs = self.host_views(n)
+        nb = self.page_bytes(n) - (2 * n * self.cfg.num_kv_heads * 4 if self.cfg.kv_dtype == "fp8" else 0)
+        d, h = self.dev_flat[:nb], self.host_flat[:nb]
+        return {
+            "offload": self._time(lambda: ckv.kv_pages_offload(self.pool, pg, hk, hv, hks, hvs,
+                                                               staging=self.staging), reps, warmup),
+            "reload": self._time(lambda: ckv.kv_pages_reload(self.pool, pg, hk, hv, hks, hvs,
+                                                             staging=self.staging), reps, warmup),
+            "copy_d2h": self._time(lambda: h.copy_(d, non_blocking=True), reps, warmup),
+            "copy_h2d": self._time(lambda: d.copy_(h, non_blocking=True), reps, warmup),
+        }
+
+
+def transfer_profile(cfg, page_counts: Sequence[int], reps: int = 5) -> dict:
+    """GB/s of offload / reload per page count (the paper's item (1)), with
+    the plain pinned copy of the same bytes alongside."""
+    timer = TransferTimer(cfg, max(page_counts))
+    res = {"config": cfg.name, "page_counts": list(page_counts), "bytes": [], "ms": {}, "gbps": {}}
+    for n in page_counts:
+        t = timer.time(n, reps=reps)
+        nb = timer.page_bytes(n)
+        res["bytes"].append(nb)
+        for key, ms in t.items():
+            res["ms"].setdefault(key, []).append(ms)
+            res["gbps"].setdefault(key, []).append(nb / (ms * 1e-3) / 1e9)
+        print(f"[transfer] pages={n:6d} ({nb / 2**20:8.1f} MiB): " +
+              "  ".join(f"{k} {nb / (v * 1e-3) / 1e9:6.1f} GB/s" for k, v in t.items()),
+              file=sys.stderr, flush=True)
+    res["fit"] = {key: fit_linear(res["bytes"], ms) for key, ms in res["ms"].items()}
+    for key, f in res["fit"].items():
+        print(f"[transfer] fit {key:8s}: {f['gbps']:6.1f} GB/s + {f['t0_us']:6.1f} us  (R^2 {f['r2']:.6f})",
+              file=sys.stderr, flush=True)
+    return res
+
+
 def profile(cfg, max_len: int, chunks: Sequence[int], first: int = 1000, reps: int = 3,
             window: int = 0) -> dict:
     timer = PrefillTimer(cfg, max_len, window=window)
@@ -155,8 +287,14 @@ def main(argv=None):
     ap.add_argument("--chunks", type=int, nargs="*", default=[256, 512, 1024, 2048, 4096])
     ap.add_argument("--window", type=int, default=0)
     ap.add_argument("--reps", type=int, default=3)
+    ap.add_argument("--transfer", action="store_true",
+                    help="profile host-link page offload/reload instead of prefill")
+    ap.add_argument("--pages", type=int, nargs="*", default=[16, 64, 256, 1024, 4096, 16384])
     args = ap.parse_args(argv)
     cfg = workload.CONFIGS[args.config]
+    if args.transfer:
+        print(json.dumps(transfer_profile(cfg, args.pages, max(args.reps, 3))))
+        return
     print(json.dumps(profile(cfg, args.max_len, args.chunks, args.first, args.reps, args.window)))
 
 

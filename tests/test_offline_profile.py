@@ -72,3 +72,25 @@ def test_small_sweep_on_gpu_and_chunk_view_parity():
     assert all(t > 0 for t in ms)
     assert ms[-1] > ms[0]
     assert op.fit_quadratic(lengths, ms)["r2"] > 0.9
+
+
+@pytest.mark.gpu
+def test_transfer_profile_small():
+    import workload
+
+    cfg = workload.Config("prof", 5, 16, 4, 128, 16, "bf16", "bf16")
+    res = op.transfer_profile(cfg, [8, 64], reps=3)
+    assert res["bytes"] == [2 * n * 4 * 16 * 128 * 2 for n in (8, 64)]
+    for key in ("offload", "reload", "copy_d2h", "copy_h2d"):
+        assert all(g > 0 for g in res["gbps"][key])
+
+
+def test_linear_fit_recovers_bandwidth_and_fixed_cost():
+    x = np.array([1e6, 4e6, 16e6, 64e6])
+    t = 0.025 + x / 56e9 * 1e3  # ms: 25 us + bytes at 56 GB/s
+    f = op.fit_linear(x, t)
+    assert f["gbps"] == pytest.approx(56.0, rel=1e-9)
+    assert f["t0_us"] == pytest.approx(25.0, rel=1e-9)
+    assert f["r2"] == pytest.approx(1.0, abs=1e-12)
+    with pytest.raises(ValueError):
+        op.fit_linear([1.0], [1.0])
