@@ -618,9 +618,9 @@ int prefill_block_keys(int d, bool fp8) { return d >= 256 && fp8 ? 32 : 64; }
 
 }  // namespace
 
-// Key partitions per row tile: one while the row tiles alone fill the GPU
-// (twice the resident workgroups); otherwise enough to fill it, with at
-// least 1024 keys per partition and at most 32 partitions.
+// Key partitions per row tile: one while the row tiles fill at least half
+// of the resident workgroup slots; otherwise about enough for one full
+// wave, with at least 2048 keys per partition and at most 32 partitions.
 void prefill_splits(const PoolView &p, const BatchView &b, int h_q, int *splits, int *split_len) {
   const int group = h_q / p.h_kv;
   const long long tiles = ((long long)b.max_q * group + kRows - 1) / kRows;
@@ -628,10 +628,12 @@ void prefill_splits(const PoolView &p, const BatchView &b, int h_q, int *splits,
   const long long slots = (p.d >= 256 ? 1 : 2) * 256;
   const long long max_kv = (long long)b.max_ctx + b.max_q;
   const int bn = prefill_block_keys(p.d, p.kv_dtype == 2);
+  // Each split costs every row an fp32 (D + 2)-float partial, written and
+  // read back by the merge, which a short key range does not repay.
   long long s = 1;
-  if (items > 0 && items < 2 * slots) {
-    s = (2 * slots + items - 1) / items;
-    s = std::min<long long>(s, (max_kv + 1023) / 1024);
+  if (items > 0 && 2 * items <= slots) {
+    s = (slots + items - 1) / items;
+    s = std::min<long long>(s, (max_kv + 2047) / 2048);
     s = std::max<long long>(std::min<long long>(s, 32), 1);
   }
   long long len = (max_kv + s - 1) / s;
