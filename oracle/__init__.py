@@ -10,5 +10,6 @@ Modules:
   formats  bfloat16 and fp8 E4M3FN encode/decode from their definitions
   paged    append, gather, dense softmax attention, LSE merge (NumPy fp64)
   brute    pure-Python loops for tiny inputs, used to pin `paged`
+  ttl      the TTL control plane (Eq. 2, cold start, eta, Alg. 1) in plain Python
 """
-from . import brute, formats, paged  # noqa: F401
+from . import brute, formats, paged, ttl  # noqa: F401

@@ -82,3 +82,62 @@ def test_dropped_max_subtraction_overflows_where_oracle_does_not():
     out = paged.attend(q, np.array([2]), k, v, 1.0, 0)
     w = np.exp(np.array([1000.0, 1001.0, 999.0]) - 1001.0)
     assert np.allclose(out[0, 0], (w @ v[:, 0]) / w.sum(), atol=1e-14)
+
+
+# ---------------------------------------------------------------- TTL oracle
+
+def _ttl_pins_hold():
+    """The TTL oracle's worked examples and closed forms (see test_ttl.py)."""
+    import math
+
+    from oracle import ttl
+
+    grid = np.linspace(0.0, 12.0, 12001)
+    ok = ttl.eq2_ttl([1.0, 2.0, 3.0, 10.0], 5.0) == 3.0
+    ok &= ttl.eq2_ttl([1.0, 1.0, 1.0, 4.0], 2.0) == 1.0
+    ok &= ttl.eq2_ttl([2.0, 4.0], 4.0) == 0.0
+    for B in (0.5, 2.0, 10.0):
+        best = grid[np.argmax((1.0 - np.exp(-grid)) * B - grid)]
+        ok &= abs(ttl.cold_ttl(B) - best) < 2e-3
+    ok &= abs(ttl.memoryfulness([5] * 10) - 1.0) < 1e-12
+    ok &= abs(ttl.memoryfulness([1, 3]) - 5.0 / 11.0) < 1e-12
+    return bool(ok) and math.isfinite(ttl.cold_ttl(2.0))
+
+
+def test_unmutated_ttl_oracle_agrees():
+    assert _ttl_pins_hold()
+
+
+@pytest.mark.parametrize("name, mutant", [
+    ("cdf", lambda S, tau: sum(1 for t in S if t < tau) / len(S)),          # strict: misses the step
+    ("cold_ttl", lambda B: max(0.0, np.log(B) - 1.0) if B > 0 else 0.0),      # shifted optimum
+    ("cold_ttl", lambda B: max(0.0, np.log(2.0 * B)) if B > 0 else 0.0),      # lost factor
+])
+def test_ttl_formula_mutants_are_caught(monkeypatch, name, mutant):
+    from oracle import ttl
+
+    monkeypatch.setattr(ttl, name, mutant)
+    assert not _ttl_pins_hold()
+
+
+def test_memoryfulness_sign_mutant_is_caught(monkeypatch):
+    from oracle import ttl
+
+    real = ttl.memoryfulness
+    monkeypatch.setattr(ttl, "memoryfulness", lambda Ns: -real(Ns))   # Corr instead of -Corr
+    assert not _ttl_pins_hold()
+
+
+def test_eq2_candidate_mutant_is_caught(monkeypatch):
+    from oracle import ttl
+
+    def no_zero(S, B):  # forgets the tau = 0 candidate
+        best_tau, best = None, None
+        for tau in sorted(set(S)):
+            val = ttl.cdf(S, tau) * B - tau
+            if best is None or val > best:
+                best_tau, best = tau, val
+        return best_tau
+
+    monkeypatch.setattr(ttl, "eq2_ttl", no_zero)
+    assert not _ttl_pins_hold()
