@@ -227,7 +227,28 @@ struct Tile {
   int pg[C::DPW];          // page ids of the block being issued
   uint32_t loff[C::DPW];   // per-lane load offsets
   int g, t, ipos, i_min, i_max, kv_end, kb_begin, nblk, half, col, gq, li;
+  // per-lane LDS byte offsets within a bf16 block: V^T reads of output tile
+  // dt (keys 8 (gq / 2) + li / 4, plus 32 tt + 16 ks and 4 for the second
+  // read) and K reads of k-step ds (key pi(col), plus 32 tt).  The swizzles
+  // depend on key & 15 (K) and key & 3 (V) only, so the tt / ks parts are
+  // plain immediates and the loop does no address arithmetic.
+  int offv[C::DT], offk[C::DS];
 };
+
+template <class C>
+__device__ __forceinline__ void lds_offsets(Tile<C> &T) {
+  const int key0 = 8 * (T.gq >> 1) + (T.li >> 2);
+  const int dsub = 16 * (T.gq & 1) + 4 * (T.li & 3);
+#pragma unroll
+  for (int dt = 0; dt < C::DT; ++dt) {
+    const int byte = 2 * (32 * dt + dsub);
+    T.offv[dt] = key0 * C::ROW + (((byte >> 4) ^ swz_v<C::CH>(key0)) << 4) + (byte & 15);
+  }
+  const int key = pi_row(T.col);
+#pragma unroll
+  for (int ds = 0; ds < C::DS; ++ds)
+    T.offk[ds] = key * C::ROW + (((2 * ds + T.half) ^ swz_k<C::CH>(key)) << 4);
+}
 
 // Part P (0 or 1) of S^T = K Q^T for one block: k-steps [P DS/2, (P+1) DS/2)
 // of every tile, so that each half can be scheduled against a different
@@ -239,9 +260,7 @@ __device__ __forceinline__ void qk_part(const lds_u8 *kb, const Tile<C> &T, f32x
   for (int n = 0; n < C::NQK / 2; ++n) {
     const int tt = n % C::NT, ds = P * (C::DS / 2) + n / C::NT;
     if (ds == 0) s[tt] = f32x16{};
-    const int key = 32 * tt + pi_row(T.col);
-    const int sw = swz_k<C::CH>(key);
-    const u32x4 kx = lds_ld16(kb + key * C::ROW + (((2 * ds + T.half) ^ sw) << 4));
+    const u32x4 kx = lds_ld16(kb + T.offk[ds] + 32 * tt * C::ROW);
     s[tt] = mfma32x32x16(as_bf16x8(kx), T.qf[ds], s[tt]);
   }
 }
@@ -340,19 +359,13 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32
       }
       // transposed V reads: 16-lane group gq covers columns 16(gq&1) + 0..15
       // of a 32-column tile and keys key0 .. key0+3 (key0+4 .. +7 on the
-      // second read); lane li of the group addresses key key0 + li/4,
-      // columns 4(li%4) .. +3.
-      const int key0 = 32 * tt + 16 * ks + 8 * (T.gq >> 1) + (T.li >> 2);
-      const int dsub = 16 * (T.gq & 1) + 4 * (T.li & 3);
-      const lds_u8 *r0 = vb + key0 * C::ROW;
-      const lds_u8 *r1 = r0 + 4 * C::ROW;
-      const int sw0 = swz_v<C::CH>(key0), sw1 = swz_v<C::CH>(key0 + 4);
+      // second read, same swizzle); lane li of the group addresses key
+      // key0 + li/4, columns 4(li%4) .. +3.
 #pragma unroll
       for (int dt = 0; dt < C::DT; ++dt) {
-        const int byte = 2 * (32 * dt + dsub);
-        const int cidx = byte >> 4, within = byte & 15;
-        const u32x2 lo = ds_read_tr16(r0 + ((cidx ^ sw0) << 4) + within);
-        const u32x2 hi = ds_read_tr16(r1 + ((cidx ^ sw1) << 4) + within);
+        const lds_u8 *r0 = vb + T.offv[dt] + (32 * tt + 16 * ks) * C::ROW;
+        const u32x2 lo = ds_read_tr16(r0);
+        const u32x2 hi = ds_read_tr16(r0 + 4 * C::ROW);
         const u32x4 vx = {lo.x, lo.y, hi.x, hi.y};
         T.o[dt] = mfma32x32x16(as_bf16x8(vx), as_bf16x8(pb), T.o[dt]);
       }
@@ -467,6 +480,7 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   T.col = lane & 31;
   T.gq = lane >> 4;
   T.li = lane & 15;
+  lds_offsets<C>(T);
   T.g = g;
   T.t = __builtin_amdgcn_readfirstlane(wave >> 1);
   const int Rw = R0 + wave * 32 + T.col;
