@@ -49,7 +49,11 @@
  *
  * Supported combinations: (q, pool) dtypes (F32, F32), (BF16, BF16) and
  * (BF16, FP8_E4M3); head_dim in {64, 128, 256}; page_size in {16, 64};
- * num_q_heads a multiple of num_kv_heads.
+ * num_q_heads a multiple of num_kv_heads.  Size limits (launch grids):
+ * num_seqs <= 65535 and num_q_heads <= 65535; for prefix_prefill_attn also
+ * ceil(max_q_len * num_q_heads / num_kv_heads / 128) <= 65535 and
+ * total_q_len * num_q_heads < 2^31.  Beyond them a call returns
+ * CKV_ERR_UNSUPPORTED and launches nothing.
  */
 #ifndef CKV_H
 #define CKV_H

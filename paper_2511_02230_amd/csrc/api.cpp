@@ -14,6 +14,10 @@ namespace {
 using ckv::BatchView;
 using ckv::PoolView;
 
+// Launch grids put sequences (and, for the fp32 path, query heads) in grid
+// dimensions limited to 65535 workgroups.
+constexpr long long kGridYZ = 65535;
+
 bool supported_dim(int d) { return d == 64 || d == 128 || d == 256; }
 bool supported_page(int ps) { return ps == 16 || ps == 64; }
 bool valid_dtype(int t) { return t == CKV_F32 || t == CKV_BF16 || t == CKV_FP8_E4M3; }
@@ -34,6 +38,7 @@ ckv_status_t check_batch(const ckv_pool_t *p, const ckv_batch_t *b, int mode) {
   if (b->num_seqs < 0 || b->total_q_len < 0 || b->max_q_len < 0 || b->max_ctx_len < 0)
     return CKV_ERR_INVALID_ARG;
   if (b->num_seqs == 0) return CKV_OK;
+  if (b->num_seqs > kGridYZ) return CKV_ERR_UNSUPPORTED;
   if (b->max_pages_per_seq <= 0 || !b->block_table || !b->ctx_lens) return CKV_ERR_INVALID_ARG;
   const long long cap = (long long)b->max_pages_per_seq * p->page_size;
   if (mode == 0) {
@@ -48,6 +53,17 @@ ckv_status_t check_batch(const ckv_pool_t *p, const ckv_batch_t *b, int mode) {
 
 ckv_status_t check_heads(const ckv_pool_t *p, int num_q_heads) {
   if (num_q_heads <= 0 || num_q_heads % p->num_kv_heads != 0) return CKV_ERR_INVALID_ARG;
+  if (num_q_heads > kGridYZ) return CKV_ERR_UNSUPPORTED;
+  return CKV_OK;
+}
+
+// Prefill grid: row tiles of the longest new turn in grid.y, and the merge
+// of key partitions over total_q_len * num_q_heads rows in grid.x.
+ckv_status_t check_prefill_grid(const ckv_pool_t *p, const ckv_batch_t *b, int num_q_heads) {
+  const long long rows = (long long)b->max_q_len * (num_q_heads / p->num_kv_heads);
+  const long long tiles = (rows + ckv::prefill_rows_per_tile() - 1) / ckv::prefill_rows_per_tile();
+  if (tiles > kGridYZ) return CKV_ERR_UNSUPPORTED;
+  if ((long long)b->total_q_len * num_q_heads > INT_MAX) return CKV_ERR_UNSUPPORTED;
   return CKV_OK;
 }
 
@@ -131,6 +147,7 @@ size_t prefix_prefill_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t 
       check_heads(pool, num_q_heads) != CKV_OK)
     return 0;
   if (batch->num_seqs == 0 || batch->total_q_len == 0 || pool->kv_dtype == CKV_F32) return 0;
+  if (check_prefill_grid(pool, batch, num_q_heads) != CKV_OK) return 0;
   return ckv::prefill_workspace_bytes(view(pool), view(batch), num_q_heads);
 }
 
@@ -145,6 +162,7 @@ ckv_status_t prefix_prefill_attn(const ckv_pool_t *pool, const ckv_batch_t *batc
   if (!std::isfinite(softmax_scale) || window < 0) return CKV_ERR_INVALID_ARG;
   if (batch->num_seqs == 0 || batch->total_q_len == 0) return CKV_OK;
   if (!q || !out) return CKV_ERR_INVALID_ARG;
+  CKV_TRY(check_prefill_grid(pool, batch, num_q_heads));
   if (q_dtype == CKV_F32)
     return launched(ckv::launch_attn_f32(view(pool), view(batch), static_cast<const float *>(q),
                                          num_q_heads, softmax_scale, window, false,

@@ -27,6 +27,7 @@ hipError_t launch_attn_f32(const PoolView &p, const BatchView &b, const float *q
                            float scale, int window, bool decode, float *out, hipStream_t s);
 
 size_t prefill_workspace_bytes(const PoolView &p, const BatchView &b, int h_q);
+int prefill_rows_per_tile();  // query rows (token x head of a group) per prefill workgroup
 hipError_t launch_prefill_bf16(const PoolView &p, const BatchView &b, const void *q, int h_q,
                                float scale, int window, void *out, void *ws, hipStream_t s);
 

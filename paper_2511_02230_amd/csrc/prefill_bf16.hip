@@ -632,6 +632,8 @@ int prefill_block_keys(int d, bool fp8) { return d >= 256 && fp8 ? 32 : 64; }
 
 }  // namespace
 
+int prefill_rows_per_tile() { return kRows; }
+
 // Key partitions per row tile: one while the row tiles fill at least half
 // of the resident workgroup slots; otherwise about enough for one full
 // wave, with at least 2048 keys per partition and at most 32 partitions.
