@@ -300,15 +300,11 @@ __device__ __forceinline__ void scale_mask(const PrefillArgs &a, const int32_t *
   }
 }
 
-// Softmax of block j (scores s after scale_mask) and O^T += V^T P^T with V
-// of block j (bf16 layout at vb).  The two halves of the next block's S^T
-// are issued around the row maximum, and before the exponentials.
-template <class C, int PS, bool FP8>
-__device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32x16 (&s)[C::NT],
-                                           const float (&vsc)[C::NT * 2], const lds_u8 *vb,
-                                           const lds_u8 *kb_next, f32x16 (&s_next)[C::NT]) {
-  __builtin_amdgcn_s_setprio(1);
-  qk_part<C, 0>(kb_next, T, s_next);
+// Row maximum of block j's scores in log2 units (both halves of the wave),
+// and the lazy move of the reference maximum: only when the block's maximum
+// exceeds it by more than the slack; O and l are then rescaled.
+template <class C, bool FP8>
+__device__ __forceinline__ void bump_max(const PrefillArgs &a, Tile<C> &T, const f32x16 (&s)[C::NT]) {
   float mx = kNegInf;
 #pragma unroll
   for (int tt = 0; tt < C::NT; ++tt)
@@ -316,7 +312,6 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32
     for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[tt][e]);
   if constexpr (!FP8) mx *= a.scale_log2;  // scores stay unscaled until the exp
   mx = half_swap_max(mx);
-  // move the reference maximum only when it grows by more than the slack
   const bool bump = mx > T.m + kRescaleSlack;
   if (__builtin_amdgcn_ballot_w64(bump)) {
     // lanes that keep their reference scale by 1 (their m may still be -inf
@@ -327,48 +322,102 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt) T.o[dt] *= alpha;
   }
-  const float m_use = T.m == kNegInf ? 0.f : T.m;
+}
 
-  // second half of the next block's S^T, independent of everything below
-  qk_part<C, 1>(kb_next, T, s_next);
+// O^T += V^T P^T for one 16-key slice (tile tt, half ks) of block j with the
+// packed bf16 probabilities pb of that slice.  Transposed V reads: 16-lane
+// group gq covers columns 16(gq&1) + 0..15 of a 32-column tile and keys
+// key0 .. key0+3 (key0+4 .. +7 on the second read, same swizzle); lane li of
+// the group addresses key key0 + li/4, columns 4(li%4) .. +3.
+template <class C>
+__device__ __forceinline__ void pv_slice(Tile<C> &T, const lds_u8 *vb, int tt, int ks, const u32x4 &pb) {
+#pragma unroll
+  for (int dt = 0; dt < C::DT; ++dt) {
+    const lds_u8 *r0 = vb + T.offv[dt] + (32 * tt + 16 * ks) * C::ROW;
+    const u32x2 lo = ds_read_tr16(r0);
+    const u32x2 hi = ds_read_tr16(r0 + 4 * C::ROW);
+    const u32x4 vx = {lo.x, lo.y, hi.x, hi.y};
+    T.o[dt] = mfma32x32x16(as_bf16x8(vx), as_bf16x8(pb), T.o[dt]);
+  }
+}
 
-  // ---- P = exp2(scale * s - m); O^T += V^T P^T
+// bf16 pools: P = exp2(scale * s - m) for the whole block, packed to bf16,
+// and this lane's part of the block's row sum (the bf16 values the MFMA
+// consumes, two at a time).
+template <class C>
+__device__ __forceinline__ float exp_block(const PrefillArgs &a, const f32x16 (&s)[C::NT], float m,
+                                           u32x4 (&pb)[C::NT * 2]) {
+  float lb = 0.f;
 #pragma unroll
-  for (int tt = 0; tt < C::NT; ++tt) {
+  for (int q = 0; q < C::NT * 2; ++q) {
+    float p[8];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int e = 0; e < 8; ++e) p[e] = fast_exp2(__builtin_fmaf(s[q >> 1][8 * (q & 1) + e], a.scale_log2, -m));
+    pb[q] = u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                  pack_bf16x2(p[6], p[7])};
+    lb = add_bf16x2(pb[q].x, lb);
+    lb = add_bf16x2(pb[q].y, lb);
+    lb = add_bf16x2(pb[q].z, lb);
+    lb = add_bf16x2(pb[q].w, lb);
+  }
+  return lb;
+}
+
+// Softmax of block j (scores s after scale_mask) and O^T += V^T P^T with V
+// of block j (bf16 layout at vb).  The two halves of the next block's S^T
+// are issued around the exponentials.
+//
+// bf16 pools skip the row maximum on most blocks: the exponentials are taken
+// against the current reference maximum first.  Every probability is at most
+// the block's row sum, so a sum of at most 2^slack (on both halves) shows
+// that no score rose more than the slack above the reference, the case in
+// which the maximum would not move anyway.  Otherwise (a larger or
+// non-finite sum, e.g. while a row has seen no key and its reference is
+// -inf) the block is redone the reduced way: row maximum, possible move of
+// the reference with the rescale of O and l, exponentials again.  The
+// reference maximum therefore follows the same rule as on the reduced path,
+// block by block.
+// fp8 pools reduce the maximum first on every block (the key scale varies
+// per page and multiplies each score before the exponential).
+template <class C, int PS, bool FP8>
+__device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32x16 (&s)[C::NT],
+                                           const float (&vsc)[C::NT * 2], const lds_u8 *vb,
+                                           const lds_u8 *kb_next, f32x16 (&s_next)[C::NT]) {
+  __builtin_amdgcn_s_setprio(1);
+  if constexpr (!FP8) {
+    constexpr float kSlackSum = 256.f;  // 2^kRescaleSlack
+    static_assert(kRescaleSlack == 8.0f, "kSlackSum is 2^kRescaleSlack");
+    u32x4 pb[C::NT * 2];
+    qk_part<C, 0>(kb_next, T, s_next);
+    float lb = exp_block<C>(a, s, T.m, pb);
+    // second half of the next block's S^T, independent of the softmax
+    qk_part<C, 1>(kb_next, T, s_next);
+    if (__builtin_amdgcn_ballot_w64(!(lb <= kSlackSum))) {
+      bump_max<C, FP8>(a, T, s);
+      lb = exp_block<C>(a, s, T.m == kNegInf ? 0.f : T.m, pb);
+    }
+    T.l += lb;
+#pragma unroll
+    for (int q = 0; q < C::NT * 2; ++q) pv_slice<C>(T, vb, q >> 1, q & 1, pb[q]);
+  } else {
+    qk_part<C, 0>(kb_next, T, s_next);
+    bump_max<C, FP8>(a, T, s);
+    const float m_use = T.m == kNegInf ? 0.f : T.m;
+    // second half of the next block's S^T, independent of everything below
+    qk_part<C, 1>(kb_next, T, s_next);
+    // P = exp2(k_scale * scale * s - m) v_scale; O^T += V^T P^T
+#pragma unroll
+    for (int q = 0; q < C::NT * 2; ++q) {
       float p[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float x = s[tt][8 * ks + e];
-        if constexpr (FP8) {
-          p[e] = fast_exp2(x - m_use);
-          T.l += p[e];
-          p[e] *= vsc[2 * tt + ks];
-        } else {
-          p[e] = fast_exp2(__builtin_fmaf(x, a.scale_log2, -m_use));
-        }
+        p[e] = fast_exp2(s[q >> 1][8 * (q & 1) + e] - m_use);
+        T.l += p[e];
+        p[e] *= vsc[q];
       }
       const u32x4 pb = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
                         pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
-      if constexpr (!FP8) {
-        T.l = add_bf16x2(pb.x, T.l);
-        T.l = add_bf16x2(pb.y, T.l);
-        T.l = add_bf16x2(pb.z, T.l);
-        T.l = add_bf16x2(pb.w, T.l);
-      }
-      // transposed V reads: 16-lane group gq covers columns 16(gq&1) + 0..15
-      // of a 32-column tile and keys key0 .. key0+3 (key0+4 .. +7 on the
-      // second read, same swizzle); lane li of the group addresses key
-      // key0 + li/4, columns 4(li%4) .. +3.
-#pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt) {
-        const lds_u8 *r0 = vb + T.offv[dt] + (32 * tt + 16 * ks) * C::ROW;
-        const u32x2 lo = ds_read_tr16(r0);
-        const u32x2 hi = ds_read_tr16(r0 + 4 * C::ROW);
-        const u32x4 vx = {lo.x, lo.y, hi.x, hi.y};
-        T.o[dt] = mfma32x32x16(as_bf16x8(vx), as_bf16x8(pb), T.o[dt]);
-      }
+      pv_slice<C>(T, vb, q >> 1, q & 1, pb);
     }
   }
   __builtin_amdgcn_s_setprio(0);
