@@ -31,8 +31,10 @@
 //     maximum only when the block's row sum shows that it may move.  Below
 //     head_dim 256 they also carry the softmax scale in Q (rounded to bf16
 //     once) and start every S^T accumulation from minus the reference, so a
-//     score costs one exp and no FMA.  Masking only on blocks that straddle
-//     the causal diagonal or the window edge.
+//     score costs one exp and no FMA.  fp8 pools take the same lazy way with
+//     the key scale in the FMA and the value scale in the exponent's bias.
+//     Masking only on blocks that straddle the causal diagonal or the window
+//     edge.
 #include <algorithm>
 
 #include "common.hpp"
@@ -282,11 +284,14 @@ __device__ __forceinline__ void qk_part(const lds_u8 *kb, const Tile<C> &T, f32x
   }
 }
 
-// fp8 key scales and the causal / window mask of block j's scores (the
-// mask only on blocks that straddle the diagonal or the window edge).
+// fp8 scales of block j's 16-key slices (key scale times the softmax scale
+// in log2 units, and the value scale) and the causal / window mask of its
+// scores (the mask only on blocks that straddle the diagonal or the window
+// edge).  The scores stay unscaled.
 template <class C, int PS, bool FP8>
 __device__ __forceinline__ void scale_mask(const PrefillArgs &a, const int32_t *bt, const Tile<C> &T,
-                                           int j, f32x16 (&s)[C::NT], float (&vsc)[C::NT * 2]) {
+                                           int j, f32x16 (&s)[C::NT], float (&ksc)[C::NT * 2],
+                                           float (&vsc)[C::NT * 2]) {
   constexpr int BN = C::BN_;
   const int kbase = (T.kb_begin + j) * BN;
   const int half = T.half;
@@ -295,10 +300,8 @@ __device__ __forceinline__ void scale_mask(const PrefillArgs &a, const int32_t *
     for (int q = 0; q < C::NT * 2; ++q) {
       const int kp = min(kbase + 16 * q, T.kv_end - 1);
       const int idx = ldc(bt, (int)((uint32_t)kp / PS)) * a.h_kv + T.g;
-      const float ksc = a.scale_log2 * ldc(a.k_scale, idx);
+      ksc[q] = a.scale_log2 * ldc(a.k_scale, idx);
       vsc[q] = ldc(a.v_scale, idx);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s[q >> 1][8 * (q & 1) + e] *= ksc;
     }
   }
   const int W = a.window;
@@ -406,8 +409,8 @@ __device__ __forceinline__ float exp_block(const f32x16 (&s)[C::NT], float scale
 // per page and multiplies each score before the exponential).
 template <class C, int PS, bool FP8>
 __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32x16 (&s)[C::NT],
-                                           const float (&vsc)[C::NT * 2], const lds_u8 *vb,
-                                           const lds_u8 *kb_next, f32x16 (&s_next)[C::NT]) {
+                                           const float (&ksc)[C::NT * 2], const float (&vsc)[C::NT * 2],
+                                           const lds_u8 *vb, const lds_u8 *kb_next, f32x16 (&s_next)[C::NT]) {
   __builtin_amdgcn_s_setprio(1);
   if constexpr (!FP8) {
     constexpr float kSlackSum = 256.f;  // 2^kRescaleSlack
@@ -439,25 +442,66 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32
 #pragma unroll
     for (int q = 0; q < C::NT * 2; ++q) pv_slice<C>(T, vb, q >> 1, q & 1, pb[q]);
   } else {
+    constexpr float kSlackSum = 256.f;  // 2^kRescaleSlack
+    // The value scale rides in the exponent: P v_scale = exp2(k_scale scale s
+    // - m + log2 v_scale), one FMA and one exp per score; the slice's row
+    // sum divided by v_scale is its part of l.  Needs positive, finite
+    // scales (a page of zeros has scale 0: such blocks take the reduced way).
+    bool pos = true;
+    float bias[C::NT * 2], ivs[C::NT * 2];
+#pragma unroll
+    for (int q = 0; q < C::NT * 2; ++q) {
+      pos &= (ksc[q] > 0.f) & (ksc[q] <= 3.0e38f) & (vsc[q] > 0.f) & (vsc[q] <= 3.0e38f);
+      bias[q] = __builtin_amdgcn_logf(vsc[q]) - T.m;
+      ivs[q] = __builtin_amdgcn_rcpf(vsc[q]);
+    }
+    u32x4 pb[C::NT * 2];
     qk_part<C, 0>(kb_next, T, s_next);
-    bump_max<C, FP8>(a, T, s);
-    const float m_use = T.m == kNegInf ? 0.f : T.m;
-    // second half of the next block's S^T, independent of everything below
-    qk_part<C, 1>(kb_next, T, s_next);
-    // P = exp2(k_scale * scale * s - m) v_scale; O^T += V^T P^T
+    float lb = 0.f;
 #pragma unroll
     for (int q = 0; q < C::NT * 2; ++q) {
       float p[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        p[e] = fast_exp2(s[q >> 1][8 * (q & 1) + e] - m_use);
-        T.l += p[e];
-        p[e] *= vsc[q];
-      }
-      const u32x4 pb = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
-                        pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
-      pv_slice<C>(T, vb, q >> 1, q & 1, pb);
+      for (int e = 0; e < 8; ++e) p[e] = fast_exp2(__builtin_fmaf(s[q >> 1][8 * (q & 1) + e], ksc[q], bias[q]));
+      pb[q] = u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                    pack_bf16x2(p[6], p[7])};
+      float ss = add_bf16x2(pb[q].x, 0.f);
+      ss = add_bf16x2(pb[q].y, ss);
+      ss = add_bf16x2(pb[q].z, ss);
+      ss = add_bf16x2(pb[q].w, ss);
+      lb = __builtin_fmaf(ss, ivs[q], lb);
     }
+    // second half of the next block's S^T, independent of the softmax
+    qk_part<C, 1>(kb_next, T, s_next);
+    if (!pos || __builtin_amdgcn_ballot_w64(!(lb <= kSlackSum) | (T.m == kNegInf))) {
+      // reduced way: scaled scores (masked ones stay -inf), row maximum,
+      // P = exp2(k_scale scale s - m) v_scale
+#pragma unroll
+      for (int q = 0; q < C::NT * 2; ++q)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x = s[q >> 1][8 * (q & 1) + e];
+          s[q >> 1][8 * (q & 1) + e] = x == kNegInf ? kNegInf : x * ksc[q];
+        }
+      bump_max<C, FP8>(a, T, s);
+      const float m_use = T.m == kNegInf ? 0.f : T.m;
+      lb = 0.f;
+#pragma unroll
+      for (int q = 0; q < C::NT * 2; ++q) {
+        float p[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          p[e] = fast_exp2(s[q >> 1][8 * (q & 1) + e] - m_use);
+          lb += p[e];
+          p[e] *= vsc[q];
+        }
+        pb[q] = u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                      pack_bf16x2(p[6], p[7])};
+      }
+    }
+    T.l += lb;
+#pragma unroll
+    for (int q = 0; q < C::NT * 2; ++q) pv_slice<C>(T, vb, q >> 1, q & 1, pb[q]);
   }
   __builtin_amdgcn_s_setprio(0);
 }
@@ -505,10 +549,10 @@ __device__ __forceinline__ void step(const PrefillArgs &a, const int32_t *bt, Ti
     kb = R.k16;
     vb = R.v16;
   }
-  float vsc[C::NT * 2];
-  scale_mask<C, PS, FP8>(a, bt, T, j, s_cur, vsc);
+  float ksc[C::NT * 2], vsc[C::NT * 2];
+  scale_mask<C, PS, FP8>(a, bt, T, j, s_cur, ksc, vsc);
   // (past the last block this reads a stale K stage; the result is unused)
-  softmax_pv<C, PS, FP8>(a, T, s_cur, vsc, vb, kb, s_nxt);
+  softmax_pv<C, PS, FP8>(a, T, s_cur, ksc, vsc, vb, kb, s_nxt);
 }
 
 template <int D, int BN, bool FP8, int PS>

@@ -270,6 +270,42 @@ def test_fp8_quantizer_every_bf16_value():
         assert bad.size == 0, (scale, bad[:5], bits[bad[:5]], got[bad[:5]], ref[bad[:5]])
 
 
+@pytest.mark.parametrize("ps, which", [(16, "kv"), (64, "kv"), (16, "k"), (64, "v")])
+def test_fp8_pages_with_zero_scale(ps, which):
+    """A page of zeros carries scale 0 (its codes then decode to 0 whatever
+    they hold).  Zero key or value scales on some pages of the sequences:
+    prefill and decode still match the oracle, which decodes with the same
+    scales."""
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    cfg = cfg_of(f"z{ps}{which}", 16, 2, 128, ps, "fp8")
+    wl = workload.make_workload(cfg, prefill=[(300, 70), (0, 40)], decode=[200, 513])
+    say(f"case zero scales ps={ps} which={which}")
+    dw = DeviceWorkload(wl, "cuda")
+    sids = sorted(set(int(x) for x in wl.prefill.seq_ids) | set(int(x) for x in wl.decode.seq_ids))
+    st = OracleState(wl, sids=sids, device="cuda")
+    dw.append_prefill()
+    dw.append_decode()
+    torch.cuda.synchronize()
+    st.append_prefill()
+    st.append_decode()
+    zero = st.pages[::3]  # every third page of the selected sequences, both KV heads
+    for name in which:
+        getattr(dw.pool, f"{name}_scale")[torch.as_tensor(zero, device="cuda")] = 0.0
+        getattr(st, f"{name}_scale")[st.page_map[zero]] = 0.0
+    torch.cuda.synchronize()
+    pf, dc = wl.prefill, wl.decode
+    got = out_f64(dw.run_prefill())
+    ref = st.prefill(to_numpy(dw.q_prefill), st.rows_of(pf))
+    for b, r in ref.items():
+        check_close(got[pf.cu_q_lens[b]:pf.cu_q_lens[b + 1]], r, cfg, f"prefill seq {b}")
+    ref = st.decode(to_numpy(dw.q_decode), st.rows_of(dc))
+    for split in (0, 64):
+        got = out_f64(dw.run_decode(kv_split_len=split))
+        for b, r in ref.items():
+            check_close(got[b], r, cfg, f"decode seq {b} split {split}")
+
+
 def test_empty_and_degenerate_batches():
     from paper_2511_02230_amd import ckv
 
