@@ -137,7 +137,10 @@ __device__ __forceinline__ void dma16(const void *g, lds_u8 *dst) {
 }
 
 // Wave-uniform 64-bit base (scalar registers) plus a per-lane 32-bit byte
-// offset: no per-lane 64-bit address arithmetic.
+// offset: no per-lane 64-bit address arithmetic.  NT marks the load
+// non-temporal, for data that is read once (decode's V stream); data that
+// other workgroups re-read from L2 (prefill's K/V) keeps the default policy.
+template <bool NT = false>
 __device__ __forceinline__ void dma16_sv(const void *sbase, uint32_t voff, lds_u8 *dst) {
   // readfirstlane returns a signed int: widen each half as unsigned so the
   // low word is not sign-extended into the high word
@@ -145,9 +148,12 @@ __device__ __forceinline__ void dma16_sv(const void *sbase, uint32_t voff, lds_u
   const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)base);
   const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(base >> 32));
   const uint64_t sb = ((uint64_t)hi << 32) | (uint64_t)lo;
-  asm volatile(CKV_DMA_WAIT "global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sb),
-               "{m0}"(lds_offset(dst))
-               : "memory");
+  if constexpr (NT)
+    asm volatile(CKV_DMA_WAIT "global_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(sb), "{m0}"(lds_offset(dst))
+                 : "memory");
+  else
+    asm volatile(CKV_DMA_WAIT "global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sb), "{m0}"(lds_offset(dst))
+                 : "memory");
 }
 
 // Sum of two bf16 values packed in a dword, accumulated in fp32.
