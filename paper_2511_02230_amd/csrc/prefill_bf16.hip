@@ -27,12 +27,11 @@
 //     bf16 probabilities the MFMA consumes, two at a time.  The reference
 //     maximum only moves (and O is rescaled) when a block's maximum exceeds
 //     it by more than 2^8, which leaves the result unchanged but skips most
-//     rescales.  bf16 pools take the exponentials first and reduce the row
-//     maximum only when the block's row sum shows that it may move.  Below
-//     head_dim 256 they also carry the softmax scale in Q (rounded to bf16
-//     once) and start every S^T accumulation from minus the reference, so a
-//     score costs one exp and no FMA.  fp8 pools take the same lazy way with
-//     the key scale in the FMA and the value scale in the exponent's bias.
+//     rescales.  The exponentials are taken first, one FMA (scale and
+//     reference folded) and one exp per score, and the row maximum is
+//     reduced only when the block's row sum shows that it may move.  fp8
+//     pools take the same lazy way with the key scale in the FMA and the
+//     value scale in the exponent's addend.
 //     Masking only on blocks that straddle the causal diagonal or the window
 //     edge.
 #include <algorithm>
@@ -75,11 +74,6 @@ __device__ __forceinline__ int pi_row(int m) {
 
 template <int D, int BN, bool FP8, int PS>
 struct Cfg {
-  static constexpr bool F8 = FP8;
-  // bf16 pools below head_dim 256 fold the softmax scale into Q and the
-  // reference maximum into the S^T accumulator (head_dim 256 lacks the
-  // registers for the folded maximum)
-  static constexpr bool FOLD = !FP8 && D <= 128;
   static constexpr int ROW = D * 2;                    // bf16 bytes per key row in LDS
   static constexpr int CH = D / 8;                     // 16-byte chunks per bf16 row
   static constexpr int BN_ = BN;                       // keys per block
@@ -244,11 +238,6 @@ struct Tile {
   // depend on key & 15 (K) and key & 3 (V) only, so the tt / ks parts are
   // plain immediates and the loop does no address arithmetic.
   int offv[C::DT], offk[C::DS];
-  // bf16 pools: every S^T accumulation starts from negm = -mf in all
-  // elements, so the scores arrive already shifted by mf (the reference
-  // maximum, or 0 while the row has seen no key)
-  f32x16 negm;
-  float mf;
 };
 
 template <class C>
@@ -275,10 +264,7 @@ __device__ __forceinline__ void qk_part(const lds_u8 *kb, const Tile<C> &T, f32x
 #pragma unroll
   for (int n = 0; n < C::NQK / 2; ++n) {
     const int tt = n % C::NT, ds = P * (C::DS / 2) + n / C::NT;
-    if (ds == 0) {
-      if constexpr (C::FOLD) s[tt] = T.negm;
-      else s[tt] = f32x16{};
-    }
+    if (ds == 0) s[tt] = f32x16{};
     const u32x4 kx = lds_ld16(kb + T.offk[ds] + 32 * tt * C::ROW);
     s[tt] = mfma32x32x16(as_bf16x8(kx), T.qf[ds], s[tt]);
   }
@@ -330,8 +316,7 @@ __device__ __forceinline__ void bump_max(const PrefillArgs &a, Tile<C> &T, const
   for (int tt = 0; tt < C::NT; ++tt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[tt][e]);
-  if constexpr (C::FOLD) mx += T.mf;                  // scores arrive scaled and shifted by -mf
-  else if constexpr (!FP8) mx *= a.scale_log2;       // scores stay unscaled until the exp
+  if constexpr (!FP8) mx *= a.scale_log2;  // scores stay unscaled until the exp
   mx = half_swap_max(mx);
   const bool bump = mx > T.m + kRescaleSlack;
   if (__builtin_amdgcn_ballot_w64(bump)) {
@@ -362,25 +347,18 @@ __device__ __forceinline__ void pv_slice(Tile<C> &T, const lds_u8 *vb, int tt, i
   }
 }
 
-// bf16 pools: the block's probabilities, packed to bf16, and this lane's
-// part of the block's row sum (the bf16 values the MFMA consumes, two at a
-// time).  Folded scores (already scaled and shifted): P = exp2(s), or
-// exp2(s - d) after the fold moved by d; otherwise P = exp2(scale * s - d).
-enum ExpMode { kExpFolded, kExpFoldedShift, kExpScaled };
-template <class C, ExpMode MODE>
-__device__ __forceinline__ float exp_block(const f32x16 (&s)[C::NT], float scale, float d,
+// bf16 pools: the block's probabilities P = exp2(scale * s - m), packed to
+// bf16, and this lane's part of the block's row sum (the bf16 values the MFMA
+// consumes, two at a time).
+template <class C>
+__device__ __forceinline__ float exp_block(const f32x16 (&s)[C::NT], float scale, float m,
                                            u32x4 (&pb)[C::NT * 2]) {
   float lb = 0.f;
 #pragma unroll
   for (int q = 0; q < C::NT * 2; ++q) {
     float p[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float x = s[q >> 1][8 * (q & 1) + e];
-      if constexpr (MODE == kExpFolded) p[e] = fast_exp2(x);
-      else if constexpr (MODE == kExpFoldedShift) p[e] = fast_exp2(x - d);
-      else p[e] = fast_exp2(__builtin_fmaf(x, scale, -d));
-    }
+    for (int e = 0; e < 8; ++e) p[e] = fast_exp2(__builtin_fmaf(s[q >> 1][8 * (q & 1) + e], scale, -m));
     pb[q] = u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
                   pack_bf16x2(p[6], p[7])};
     lb = add_bf16x2(pb[q].x, lb);
@@ -404,9 +382,8 @@ __device__ __forceinline__ float exp_block(const f32x16 (&s)[C::NT], float scale
 // -inf) the block is redone the reduced way: row maximum, possible move of
 // the reference with the rescale of O and l, exponentials again.  The
 // reference maximum therefore follows the same rule as on the reduced path,
-// block by block.
-// fp8 pools reduce the maximum first on every block (the key scale varies
-// per page and multiplies each score before the exponential).
+// block by block.  fp8 pools do the same with the key scale as the FMA's
+// multiplier and the value scale in its addend.
 template <class C, int PS, bool FP8>
 __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32x16 (&s)[C::NT],
                                            const float (&ksc)[C::NT * 2], const float (&vsc)[C::NT * 2],
@@ -417,26 +394,12 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32
     static_assert(kRescaleSlack == 8.0f, "kSlackSum is 2^kRescaleSlack");
     u32x4 pb[C::NT * 2];
     qk_part<C, 0>(kb_next, T, s_next);
-    float lb = C::FOLD ? exp_block<C, kExpFolded>(s, 0.f, 0.f, pb)
-                       : exp_block<C, kExpScaled>(s, a.scale_log2, T.m, pb);
+    float lb = exp_block<C>(s, a.scale_log2, T.m, pb);
     // second half of the next block's S^T, independent of the softmax
     qk_part<C, 1>(kb_next, T, s_next);
     if (__builtin_amdgcn_ballot_w64(!(lb <= kSlackSum) | (T.m == kNegInf))) {
       bump_max<C, FP8>(a, T, s);
-      const float m_use = T.m == kNegInf ? 0.f : T.m;
-      if constexpr (C::FOLD) {
-        // move the fold to the (possibly new) reference; the next block's
-        // scores were formed against the old fold
-        const float d = m_use - T.mf;
-        lb = exp_block<C, kExpFoldedShift>(s, 0.f, d, pb);
-#pragma unroll
-        for (int tt = 0; tt < C::NT; ++tt) s_next[tt] -= d;
-        T.mf = m_use;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) T.negm[e] = -m_use;
-      } else {
-        lb = exp_block<C, kExpScaled>(s, a.scale_log2, m_use, pb);
-      }
+      lb = exp_block<C>(s, a.scale_log2, T.m == kNegInf ? 0.f : T.m, pb);
     }
     T.l += lb;
 #pragma unroll
@@ -659,19 +622,11 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   for (int s = 0; s < C::DS; ++s) {
     u32x4 x = {0u, 0u, 0u, 0u};
     if (rvalid) x = ld<u32x4>(a.q + qrow + 16 * s + 8 * T.half);
-    if constexpr (C::FOLD) {
-      // Q carries the softmax scale (in log2 units), rounded to bf16
-      const float c = a.scale_log2;
-      x = u32x4{pack_bf16x2(bf16_lo(x.x) * c, bf16_hi(x.x) * c), pack_bf16x2(bf16_lo(x.y) * c, bf16_hi(x.y) * c),
-                pack_bf16x2(bf16_lo(x.z) * c, bf16_hi(x.z) * c), pack_bf16x2(bf16_lo(x.w) * c, bf16_hi(x.w) * c)};
-    }
     T.qf[s] = as_bf16x8(x);
   }
 #pragma unroll
   for (int dt = 0; dt < C::DT; ++dt) T.o[dt] = f32x16{};
   T.m = kNegInf;
-  T.mf = 0.f;
-  T.negm = f32x16{};
   T.l = 0.f;
 
   f32x16 sA[C::NT], sB[C::NT];

@@ -306,6 +306,54 @@ def test_fp8_pages_with_zero_scale(ps, which):
             check_close(got[b], r, cfg, f"decode seq {b} split {split}")
 
 
+@pytest.mark.parametrize("d, kv, ps", [(128, "bf16", 16), (64, "bf16", 64), (256, "bf16", 16), (128, "fp8", 16)])
+def test_scores_growing_along_the_keys(d, kv, ps):
+    """Keys scaled by a factor that grows with their position, so that nearly
+    every block's maximum exceeds the reference by more than the lazy-rescale
+    slack: the kernels' reduced path (row maximum, rescale, moved fold) runs
+    on most blocks instead of a few.  bf16 pools: row t of K times 1 + t / 32
+    (rounded to bf16 in both pools); fp8 pools: the key scale of the
+    sequence's i-th page times 1 + i."""
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    cfg = cfg_of(f"grow{d}{kv}{ps}", 8, 2, d, ps, kv)
+    wl = workload.make_workload(cfg, prefill=[(700, 90), (0, 130)], decode=[900, 70])
+    say(f"case growing scores d={d} kv={kv} ps={ps}")
+    dw = DeviceWorkload(wl, "cuda")
+    sids = sorted(set(int(x) for x in wl.prefill.seq_ids) | set(int(x) for x in wl.decode.seq_ids))
+    st = OracleState(wl, sids=sids, device="cuda")
+    dw.append_prefill()
+    dw.append_decode()
+    torch.cuda.synchronize()
+    st.append_prefill()
+    st.append_decode()
+    for sid in sids:
+        pages = np.asarray(wl.seqs[sid].pages, np.int64)
+        comp = st.page_map[pages]
+        if kv == "fp8":
+            f = (1.0 + np.arange(len(pages))).astype(np.float32)[:, None]
+            st.k_scale[comp] = st.k_scale[comp] * f
+            dw.pool.k_scale[torch.as_tensor(pages, device="cuda")] = torch.as_tensor(st.k_scale[comp], device="cuda")
+        else:
+            tok = np.arange(len(pages))[:, None] * ps + np.arange(ps)[None, :]  # [page, slot]
+            f = (1.0 + tok / 32.0).astype(np.float32)[:, None, :, None]       # [page, 1, slot, 1]
+            bits = formats.bf16_bits_from_f32(formats.bf16_bits_to_f32(st.pool_k[comp]) * f)
+            st.pool_k[comp] = bits
+            dw.pool.k[torch.as_tensor(pages, device="cuda")] = (
+                torch.from_numpy(bits.view(np.int16)).to("cuda").view(torch.bfloat16))
+    torch.cuda.synchronize()
+    pf, dc = wl.prefill, wl.decode
+    got = out_f64(dw.run_prefill())
+    ref = st.prefill(to_numpy(dw.q_prefill), st.rows_of(pf))
+    for b, r in ref.items():
+        check_close(got[pf.cu_q_lens[b]:pf.cu_q_lens[b + 1]], r, cfg, f"prefill seq {b}")
+    ref = st.decode(to_numpy(dw.q_decode), st.rows_of(dc))
+    for split in (0, 128):
+        got = out_f64(dw.run_decode(kv_split_len=split))
+        for b, r in ref.items():
+            check_close(got[b], r, cfg, f"decode seq {b} split {split}")
+
+
 def test_empty_and_degenerate_batches():
     from paper_2511_02230_amd import ckv
 
