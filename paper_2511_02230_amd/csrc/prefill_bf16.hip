@@ -408,13 +408,15 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32
     constexpr float kSlackSum = 256.f;  // 2^kRescaleSlack
     // The value scale rides in the exponent: P v_scale = exp2(k_scale scale s
     // - m + log2 v_scale), one FMA and one exp per score; the slice's row
-    // sum divided by v_scale is its part of l.  Needs positive, finite
-    // scales (a page of zeros has scale 0: such blocks take the reduced way).
+    // sum divided by v_scale is its part of l.  Needs a positive, finite key
+    // scale and a value scale within 2^-100 .. 2^100, so that the slice sums
+    // neither flush nor overflow (a page of zeros has scale 0: such blocks
+    // take the reduced way).
     bool pos = true;
     float bias[C::NT * 2], ivs[C::NT * 2];
 #pragma unroll
     for (int q = 0; q < C::NT * 2; ++q) {
-      pos &= (ksc[q] > 0.f) & (ksc[q] <= 3.0e38f) & (vsc[q] > 0.f) & (vsc[q] <= 3.0e38f);
+      pos &= (ksc[q] > 0.f) & (ksc[q] <= 3.0e38f) & (vsc[q] >= 0x1p-100f) & (vsc[q] <= 0x1p100f);
       bias[q] = __builtin_amdgcn_logf(vsc[q]) - T.m;
       ivs[q] = __builtin_amdgcn_rcpf(vsc[q]);
     }

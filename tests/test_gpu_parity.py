@@ -270,17 +270,18 @@ def test_fp8_quantizer_every_bf16_value():
         assert bad.size == 0, (scale, bad[:5], bits[bad[:5]], got[bad[:5]], ref[bad[:5]])
 
 
-@pytest.mark.parametrize("ps, which", [(16, "kv"), (64, "kv"), (16, "k"), (64, "v")])
-def test_fp8_pages_with_zero_scale(ps, which):
+@pytest.mark.parametrize("ps, which, value", [(16, "kv", 0.0), (64, "kv", 0.0), (16, "k", 0.0), (64, "v", 0.0),
+                                              (16, "v", 1e-39), (64, "kv", 1e-39)])
+def test_fp8_pages_with_zero_scale(ps, which, value):
     """A page of zeros carries scale 0 (its codes then decode to 0 whatever
-    they hold).  Zero key or value scales on some pages of the sequences:
-    prefill and decode still match the oracle, which decodes with the same
-    scales."""
+    they hold); a page of tiny values a subnormal scale.  Such key or value
+    scales on some pages of the sequences: prefill and decode still match
+    the oracle, which decodes with the same scales."""
     from paper_2511_02230_amd.harness import DeviceWorkload
 
-    cfg = cfg_of(f"z{ps}{which}", 16, 2, 128, ps, "fp8")
+    cfg = cfg_of(f"z{ps}{which}{value}", 16, 2, 128, ps, "fp8")
     wl = workload.make_workload(cfg, prefill=[(300, 70), (0, 40)], decode=[200, 513])
-    say(f"case zero scales ps={ps} which={which}")
+    say(f"case scale {value} on some pages ps={ps} which={which}")
     dw = DeviceWorkload(wl, "cuda")
     sids = sorted(set(int(x) for x in wl.prefill.seq_ids) | set(int(x) for x in wl.decode.seq_ids))
     st = OracleState(wl, sids=sids, device="cuda")
@@ -291,8 +292,8 @@ def test_fp8_pages_with_zero_scale(ps, which):
     st.append_decode()
     zero = st.pages[::3]  # every third page of the selected sequences, both KV heads
     for name in which:
-        getattr(dw.pool, f"{name}_scale")[torch.as_tensor(zero, device="cuda")] = 0.0
-        getattr(st, f"{name}_scale")[st.page_map[zero]] = 0.0
+        getattr(dw.pool, f"{name}_scale")[torch.as_tensor(zero, device="cuda")] = value
+        getattr(st, f"{name}_scale")[st.page_map[zero]] = np.float32(value)
     torch.cuda.synchronize()
     pf, dc = wl.prefill, wl.decode
     got = out_f64(dw.run_prefill())
