@@ -307,8 +307,15 @@ def test_fp8_pages_with_zero_scale(ps, which, value):
             check_close(got[b], r, cfg, f"decode seq {b} split {split}")
 
 
-@pytest.mark.parametrize("d, kv, ps", [(128, "bf16", 16), (64, "bf16", 64), (256, "bf16", 16), (128, "fp8", 16)])
-def test_scores_growing_along_the_keys(d, kv, ps):
+GROW = [(128, "bf16", 16, [(700, 90), (0, 130)]), (64, "bf16", 64, [(700, 90), (0, 130)]),
+        (256, "bf16", 16, [(700, 90), (0, 130)]), (128, "fp8", 16, [(700, 90), (0, 130)]),
+        # few row tiles over a long prefix: key partitions, each with its own
+        # reference maximum, merged afterwards
+        (128, "bf16", 16, [(5000, 40)]), (128, "fp8", 64, [(5000, 40)])]
+
+
+@pytest.mark.parametrize("d, kv, ps, prefill", GROW, ids=lambda c: str(c) if not isinstance(c, list) else f"P{c[0][0]}")
+def test_scores_growing_along_the_keys(d, kv, ps, prefill):
     """Keys scaled by a factor that grows with their position, so that nearly
     every block's maximum exceeds the reference by more than the lazy-rescale
     slack: the kernels' reduced path (row maximum, rescale, moved fold) runs
@@ -318,8 +325,8 @@ def test_scores_growing_along_the_keys(d, kv, ps):
     from paper_2511_02230_amd.harness import DeviceWorkload
 
     cfg = cfg_of(f"grow{d}{kv}{ps}", 8, 2, d, ps, kv)
-    wl = workload.make_workload(cfg, prefill=[(700, 90), (0, 130)], decode=[900, 70])
-    say(f"case growing scores d={d} kv={kv} ps={ps}")
+    wl = workload.make_workload(cfg, prefill=prefill, decode=[900, 70])
+    say(f"case growing scores d={d} kv={kv} ps={ps} prefill={prefill}")
     dw = DeviceWorkload(wl, "cuda")
     sids = sorted(set(int(x) for x in wl.prefill.seq_ids) | set(int(x) for x in wl.decode.seq_ids))
     st = OracleState(wl, sids=sids, device="cuda")
