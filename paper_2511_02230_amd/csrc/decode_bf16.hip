@@ -433,7 +433,10 @@ int decode_split_len(const PoolView &p, const BatchView &b, int h_q, int request
   const int group = h_q / p.h_kv;
   const int head_chunks = (group + 15) / 16;
   const long long items = (long long)b.num_seqs * p.h_kv * head_chunks;
-  long long want = (8192 + items - 1) / std::max<long long>(items, 1);
+  // about 8192 work items of 128-wide heads; a 256-wide head moves twice the
+  // bytes per key, so half as many of its partitions make the same work
+  const long long target = p.d >= 256 ? 4096 : 8192;
+  long long want = (target + items - 1) / std::max<long long>(items, 1);
   want = std::min<long long>(std::max<long long>(want, 1), 256);
   long long len = (b.max_ctx + want - 1) / want;
   len = ((len + 255) / 256) * 256;
