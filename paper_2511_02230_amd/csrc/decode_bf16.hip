@@ -428,8 +428,8 @@ hipError_t launch(const DecodeArgs &a, int ps, int num_seqs, hipStream_t s) {
 // partitions are kept to at most 256 pages (bounds the partial buffers)
 int decode_max_split_len(int page_size) { return 256 * page_size; }
 
-int decode_split_len(const PoolView &p, const BatchView &b, int h_q, int requested) {
-  if (requested > 0) return requested;
+// Partition length for `keys` keys per sequence, at least `floor`.
+static int split_len_for(const PoolView &p, const BatchView &b, int h_q, long long keys, int floor) {
   const int group = h_q / p.h_kv;
   const int head_chunks = (group + 15) / 16;
   const long long items = (long long)b.num_seqs * p.h_kv * head_chunks;
@@ -438,10 +438,15 @@ int decode_split_len(const PoolView &p, const BatchView &b, int h_q, int request
   const long long target = p.d >= 256 ? 4096 : 8192;
   long long want = (target + items - 1) / std::max<long long>(items, 1);
   want = std::min<long long>(std::max<long long>(want, 1), 256);
-  long long len = (b.max_ctx + want - 1) / want;
+  long long len = (keys + want - 1) / want;
   len = ((len + 255) / 256) * 256;
-  len = std::max<long long>(len, 512);
+  len = std::max<long long>(len, floor);
   return (int)std::min<long long>(len, decode_max_split_len(p.ps));
+}
+
+int decode_split_len(const PoolView &p, const BatchView &b, int h_q, int requested) {
+  if (requested > 0) return requested;
+  return split_len_for(p, b, h_q, b.max_ctx, 512);
 }
 
 size_t decode_workspace_bytes(const PoolView &p, const BatchView &b, int h_q, int split_len) {
@@ -475,10 +480,9 @@ hipError_t launch_decode_bf16(const PoolView &p, const BatchView &b, const void 
   if (a.max_splits < 1) a.max_splits = 1;
   if (split_len == 0 && window > 0 && window < b.max_ctx) {
     // a sliding window sees at most `window` keys: size the partitions for
-    // that, as long as the partials still fit the workspace sized above
-    BatchView bw = b;
-    bw.max_ctx = window;
-    const int lw = decode_split_len(p, bw, h_q, 0);
+    // that (down to 256 keys: a 1024-key window then still spreads over four
+    // workgroups), as long as the partials still fit the workspace sized above
+    const int lw = split_len_for(p, b, h_q, window, 256);
     const int sw = (window + lw - 1) / lw;
     if (sw <= a.max_splits) {
       a.split_len = lw;
