@@ -157,6 +157,10 @@ SMALL = [
     (cfg_of("s1", 32, 8, 128, 16, "bf16"), [(6000, 300)], [6300], 0),
     (cfg_of("s2", 16, 8, 256, 16, "bf16"), [(5000, 100)], [5100], 700),
     (cfg_of("s3", 24, 2, 128, 64, "fp8"), [(4000, 64), (100, 20)], [4064], 0),
+    # a group of 20 query heads: prefill row tiles cut tokens mid-group, and
+    # decode covers the group in two head chunks, the second one ragged
+    (cfg_of("g1", 40, 2, 128, 16, "bf16"), [(90, 33), (0, 7)], [1, 77, 300], 0),
+    (cfg_of("g2", 40, 2, 128, 64, "fp8"), [(150, 21)], [64, 129], 0),
     (cfg_of("f1", 4, 2, 64, 16, "f32", "f32"), [(30, 20), (0, 3)], [19, 50], 0),
     (cfg_of("f2", 4, 1, 128, 64, "f32", "f32"), [(70, 9)], [129], 5),
 ]
