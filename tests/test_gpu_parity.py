@@ -366,6 +366,41 @@ def test_scores_growing_along_the_keys(d, kv, ps, prefill):
             check_close(got[b], r, cfg, f"decode seq {b} split {split}")
 
 
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+def test_loose_host_bounds(kv):
+    """max_q_len and max_ctx_len are upper bounds: looser ones launch more
+    row tiles and key partitions, the extra ones empty, and the results still
+    match the oracle."""
+    from paper_2511_02230_amd import ckv
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    cfg = cfg_of(f"loose{kv}", 16, 2, 128, 16, kv)
+    wl = workload.make_workload(cfg, prefill=[(300, 40), (20, 5)], decode=[100, 260])
+    say(f"case loose bounds kv={kv}")
+    dw = DeviceWorkload(wl, "cuda")
+    sids = sorted(set(int(x) for x in wl.prefill.seq_ids) | set(int(x) for x in wl.decode.seq_ids))
+    st = OracleState(wl, sids=sids, device="cuda")
+    dw.append_prefill()
+    dw.append_decode()
+    torch.cuda.synchronize()
+    st.append_prefill()
+    st.append_decode()
+    pf, dc = wl.prefill, wl.decode
+    cap = int(dw.prefill.block_table.shape[1]) * cfg.page_size
+    loose = dataclasses.replace(dw.prefill, max_q_len=min(cap, 3 * dw.prefill.max_q_len), max_ctx_len=cap)
+    got = out_f64(ckv.prefix_prefill_attn(dw.pool, loose, dw.q_prefill, cfg.softmax_scale, 0))
+    ref = st.prefill(to_numpy(dw.q_prefill), st.rows_of(pf))
+    for b, r in ref.items():
+        check_close(got[pf.cu_q_lens[b]:pf.cu_q_lens[b + 1]], r, cfg, f"prefill seq {b}")
+    dcap = int(dw.decode.block_table.shape[1]) * cfg.page_size
+    loose_d = dataclasses.replace(dw.decode, max_ctx_len=dcap)
+    ref = st.decode(to_numpy(dw.q_decode), st.rows_of(dc))
+    for split in (0, 64):
+        got = out_f64(ckv.paged_decode_attn(dw.pool, loose_d, dw.q_decode, cfg.softmax_scale, 0, split))
+        for b, r in ref.items():
+            check_close(got[b], r, cfg, f"decode seq {b} split {split}")
+
+
 def test_empty_and_degenerate_batches():
     from paper_2511_02230_amd import ckv
 
