@@ -731,9 +731,7 @@ int prefill_block_keys(int d, bool fp8) { return d >= 256 && fp8 ? 32 : 64; }
 
 int prefill_rows_per_tile() { return kRows; }
 
-// Key partitions per row tile: one while the row tiles fill at least half
-// of the resident workgroup slots; otherwise about enough for one full
-// wave, with at least 2048 keys per partition and at most 32 partitions.
+// Key partitions per row tile (small batches only; see below).
 void prefill_splits(const PoolView &p, const BatchView &b, int h_q, int *splits, int *split_len) {
   const int group = h_q / p.h_kv;
   const long long tiles = ((long long)b.max_q * group + kRows - 1) / kRows;
@@ -742,12 +740,24 @@ void prefill_splits(const PoolView &p, const BatchView &b, int h_q, int *splits,
   const long long max_kv = (long long)b.max_ctx + b.max_q;
   const int bn = prefill_block_keys(p.d, p.kv_dtype == 2);
   // Each split costs every row an fp32 (D + 2)-float partial, written and
-  // read back by the merge, which a short key range does not repay.
+  // read back by the merge, which a short key range does not repay: at least
+  // 2048 keys per partition, at most 32 partitions.  Among those, take the
+  // count with the fewest workgroup waves per unit of work (ties and gains
+  // under 3 % to fewer partitions): 128 tiles on 512 slots take 4, 384 take
+  // 4 (3 full waves instead of one 3/4-full wave of 4x longer ones), 768
+  // take 2 (3 waves instead of 2, each half as long).  Batches of 4 waves or
+  // more keep one partition.
   long long s = 1;
-  if (items > 0 && 2 * items <= slots) {
-    s = (slots + items - 1) / items;
-    s = std::min<long long>(s, (max_kv + 2047) / 2048);
-    s = std::max<long long>(std::min<long long>(s, 32), 1);
+  if (items > 0 && items < 4 * slots) {
+    const long long smax = std::min<long long>(32, (max_kv + 2047) / 2048);
+    double best = (double)((items + slots - 1) / slots);
+    for (long long c = 2; c <= smax; ++c) {
+      const double w = (double)((items * c + slots - 1) / slots) / (double)c;
+      if (w < 0.97 * best) {
+        best = w;
+        s = c;
+      }
+    }
   }
   long long len = (max_kv + s - 1) / s;
   len = (len + bn - 1) / bn * bn;
