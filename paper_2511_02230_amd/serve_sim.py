@@ -93,7 +93,7 @@ class CostModel:
     linear layers, 20 ms per decode step."""
 
     layers: int = 80
-    attn_ms: Tuple[float, float, float] = (1.3486e-08, 7.4140e-06, 8.1241e-02)
+    attn_ms: Tuple[float, float, float] = (1.3906e-08, 6.9167e-06, 7.7587e-02)
     linear_s_per_token: float = 2 * 70e9 / 1.2e15
     decode_s_per_token: float = 0.020
     kv_bytes_per_token: int = 80 * 2 * 8 * 128 * 2
