@@ -137,8 +137,10 @@ ckv_status_t kv_append(const ckv_pool_t *pool, const ckv_batch_t *batch,
  *   Softmax and accumulation are fp32; BF16 products run on MFMA in bf16.
  *   workspace: at least prefix_prefill_workspace_bytes(...) bytes, device
  *   memory owned by the caller and free for the duration of the call.  It is
- *   0 when the batch's row tiles fill the GPU; otherwise each tile's keys are
- *   split into partitions whose fp32 partials land there before a merge
+ *   0 when the batch's row tiles make at least four waves of workgroups on the
+ *   GPU, or when no key partitioning would cut the waves per unit of work by
+ *   3 %; otherwise each tile's keys are split into partitions (>= 2048 keys,
+ *   at most 32) whose fp32 partials land there before a merge
  *   (total_q_len * num_q_heads * partitions * (head_dim + 2) * 4 bytes).
  *   Too small a workspace returns CKV_ERR_WORKSPACE and launches nothing.
  */
