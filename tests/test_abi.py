@@ -151,3 +151,21 @@ def test_size_limits_are_rejected_before_any_launch(ckv):
     # missing workspace only if one is needed, so ask for the size instead)
     ok = _batch(ckv, max_pages_per_seq=70000, max_q_len=65535 * 16, total_q_len=65535 * 16, max_ctx_len=0)
     assert ckv.LIB.prefix_prefill_workspace_bytes(ctypes.byref(P), ctypes.byref(ok), 16) == 0
+
+
+@pytest.mark.parametrize("h_q,h_kv,d,n,prefix,splits", [
+    (64, 8, 128, 256, 65280, 4),    # 128 row tiles on 512 slots: one full wave of quarter-length work
+    (64, 8, 128, 768, 64768, 4),    # 384 tiles: three full waves instead of one 3/4-full wave
+    (64, 8, 128, 1536, 64000, 2),   # 768 tiles: three half-length waves instead of two
+    (64, 8, 128, 256, 3840, 2),     # a 4096-key context allows two partitions of >= 2048 keys
+    (64, 8, 128, 4096, 61440, 1),   # 2048 tiles: four waves or more keep one partition
+    (16, 8, 256, 256, 65280, 8),    # head_dim 256, one workgroup per CU: 32 tiles on 256 slots
+])
+def test_prefill_key_partitions(ckv, h_q, h_kv, d, n, prefix, splits):
+    """Key partitions of small prefill batches, seen through the workspace size:
+    total rows x query heads x partitions x (head_dim + 2) fp32 values, or 0 for one."""
+    P = _pool(ckv, num_pages=100000, num_kv_heads=h_kv, head_dim=d)
+    pages = (prefix + n + 15) // 16
+    B = _batch(ckv, max_pages_per_seq=pages, total_q_len=n, max_q_len=n, max_ctx_len=prefix)
+    got = ckv.LIB.prefix_prefill_workspace_bytes(ctypes.byref(P), ctypes.byref(B), h_q)
+    assert got == (0 if splits == 1 else n * h_q * splits * (d + 2) * 4)
