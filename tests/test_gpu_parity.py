@@ -157,6 +157,9 @@ SMALL = [
     (cfg_of("s1", 32, 8, 128, 16, "bf16"), [(6000, 300)], [6300], 0),
     (cfg_of("s2", 16, 8, 256, 16, "bf16"), [(5000, 100)], [5100], 700),
     (cfg_of("s3", 24, 2, 128, 64, "fp8"), [(4000, 64), (100, 20)], [4064], 0),
+    # a handful of tiles over a 40k / 70k prefix: 20 and 32 partitions (the most)
+    (cfg_of("s4", 8, 1, 128, 16, "bf16"), [(40000, 64)], [40064], 0),
+    (cfg_of("s5", 16, 2, 128, 64, "fp8"), [(70000, 32)], [70032], 0),
     # a group of 20 query heads: prefill row tiles cut tokens mid-group, and
     # decode covers the group in two head chunks, the second one ragged
     (cfg_of("g1", 40, 2, 128, 16, "bf16"), [(90, 33), (0, 7)], [1, 77, 300], 0),
