@@ -87,6 +87,11 @@ struct Cfg {
   static constexpr int DS = D / 16;                    // QK^T k-steps
   static constexpr int DT = D / 32;                    // output d-tiles
   static constexpr int NQK = NT * DS;                  // QK^T MFMAs per block
+  // Chunks in which a wave issues its loads of a step.  At head_dim 256 (one
+  // wave per SIMD) no partner wave covers the stall of a burst of 16 loads,
+  // so a third goes out after the barrier, a third after the first S^T half
+  // and the rest inside PV; with two waves per SIMD one burst is faster.
+  static constexpr int SPREAD = (D >= 256 && !FP8) ? 3 : 1;
   // two-stage K ring + two-stage V ring (+ the widened bf16 K and V blocks for fp8)
   static constexpr int LDS = 4 * RAW_BLK + (FP8 ? 2 * BLK : 0);
   static_assert(RAW_BLK % 2048 == 0, "each wave issues whole 1-KB loads");
@@ -157,7 +162,7 @@ __device__ __forceinline__ void block_pages(const int32_t *bt, int kbase, int kv
 // kv_end (last block only) are redirected to row kv_end - 1: valid, finite
 // data in the same page as the load's first row (or that row's page), which
 // the causal mask removes.
-template <class C, int PS, bool FP8>
+template <class C, int PS, bool FP8, int LO = 0, int HI = C::DPW>
 __device__ __forceinline__ void issue_block(const PrefillArgs &a, const int32_t *bt, int g, int kbase,
                                             int kv_end, const int (&pg)[C::DPW],
                                             const uint32_t (&loff)[C::DPW], lds_u8 *ring_stage) {
@@ -177,13 +182,14 @@ __device__ __forceinline__ void issue_block(const PrefillArgs &a, const int32_t 
       const uint8_t *base =
           tens + (size_t)pg[p] * page_stride + head_off + (size_t)((uint32_t)key % PS) * C::RAW_ROW;
 #pragma unroll
-      for (int i = p * DPP; i < (p + 1) * DPP; ++i) dma16_sv(base, loff[i], wdst + i * 1024);
+      for (int i = p * DPP; i < (p + 1) * DPP; ++i)
+        if (i >= LO && i < HI) dma16_sv(base, loff[i], wdst + i * 1024);
     }
   } else {
     // last block: per-load page of its first row (clamped), per-lane clamp
     const int lane = threadIdx.x & 63;
 #pragma unroll
-    for (int i = 0; i < C::DPW; ++i) {
+    for (int i = LO; i < HI; ++i) {
       const int kf = min(kbase + h * HROWS + i * C::RPD, kv_end - 1);
       const int pgi = ldc(bt, (int)((uint32_t)kf / PS));
       const uint8_t *base = tens + (size_t)pgi * page_stride + head_off;
@@ -231,6 +237,8 @@ struct Tile {
   float m, l;
   int pg[C::DPW];          // page ids of the block being issued
   uint32_t loff[C::DPW];   // per-lane load offsets
+  int kb_iss;              // first key of the block being issued (-1: none)
+  lds_u8 *dst_iss;         // its ring stage
   int g, t, ipos, i_min, i_max, kv_end, kb_begin, nblk, half, col, gq, li;
   // per-lane LDS byte offsets within a bf16 block: V^T reads of output tile
   // dt (keys 8 (gq / 2) + li / 4, plus 32 tt + 16 ks and 4 for the second
@@ -369,6 +377,18 @@ __device__ __forceinline__ float exp_block(const f32x16 (&s)[C::NT], float scale
   return lb;
 }
 
+// Loads [K DPW / SPREAD, (K + 1) DPW / SPREAD) of the block this wave issues
+// at this step (chunk 0 right after the barrier, the rest spread over the
+// step's MFMAs).
+template <class C, int PS, bool FP8, int K>
+__device__ __forceinline__ void issue_chunk(const PrefillArgs &a, const int32_t *bt, const Tile<C> &T) {
+  if constexpr (K >= 1 && K < C::SPREAD) {
+    if (T.kb_iss >= 0)
+      issue_block<C, PS, FP8, K * C::DPW / C::SPREAD, (K + 1) * C::DPW / C::SPREAD>(
+          a, bt, T.g, T.kb_iss, T.kv_end, T.pg, T.loff, T.dst_iss);
+  }
+}
+
 // Softmax of block j (scores s after scale_mask) and O^T += V^T P^T with V
 // of block j (bf16 layout at vb).  The two halves of the next block's S^T
 // are issued around the exponentials.
@@ -385,7 +405,7 @@ __device__ __forceinline__ float exp_block(const f32x16 (&s)[C::NT], float scale
 // block by block.  fp8 pools do the same with the key scale as the FMA's
 // multiplier and the value scale in its addend.
 template <class C, int PS, bool FP8>
-__device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32x16 (&s)[C::NT],
+__device__ __forceinline__ void softmax_pv(const PrefillArgs &a, const int32_t *bt, Tile<C> &T, f32x16 (&s)[C::NT],
                                            const float (&ksc)[C::NT * 2], const float (&vsc)[C::NT * 2],
                                            const lds_u8 *vb, const lds_u8 *kb_next, f32x16 (&s_next)[C::NT]) {
   __builtin_amdgcn_s_setprio(1);
@@ -394,6 +414,7 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32
     static_assert(kRescaleSlack == 8.0f, "kSlackSum is 2^kRescaleSlack");
     u32x4 pb[C::NT * 2];
     qk_part<C, 0>(kb_next, T, s_next);
+    issue_chunk<C, PS, FP8, 1>(a, bt, T);
     float lb = exp_block<C>(s, a.scale_log2, T.m, pb);
     // second half of the next block's S^T, independent of the softmax
     qk_part<C, 1>(kb_next, T, s_next);
@@ -403,7 +424,10 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, Tile<C> &T, f32
     }
     T.l += lb;
 #pragma unroll
-    for (int q = 0; q < C::NT * 2; ++q) pv_slice<C>(T, vb, q >> 1, q & 1, pb[q]);
+    for (int q = 0; q < C::NT * 2; ++q) {
+      pv_slice<C>(T, vb, q >> 1, q & 1, pb[q]);
+      if (q == 1) issue_chunk<C, PS, FP8, 2>(a, bt, T);
+    }
   } else {
     constexpr float kSlackSum = 256.f;  // 2^kRescaleSlack
     // The value scale rides in the exponent: P v_scale = exp2(k_scale scale s
@@ -483,7 +507,7 @@ struct Rings {
 // Loads issued at step j (j = -1 is the prologue): K of block j+2 by waves 0
 // and 1, V of block j+1 by waves 2 and 3.  Page ids resolve while the wave
 // waits for the previous step's loads.
-template <class C, int PS, bool FP8, int U>
+template <class C, int PS, bool FP8, int U, bool ALL = false>
 __device__ __forceinline__ void wait_and_issue(const PrefillArgs &a, const int32_t *bt, Tile<C> &T,
                                                int j, const Rings<C> &R) {
   constexpr int BN = C::BN_;
@@ -495,7 +519,16 @@ __device__ __forceinline__ void wait_and_issue(const PrefillArgs &a, const int32
   lds_barrier();
   // stage of block bi: (j + 2) & 1 = U for K, (j + 1) & 1 = U ^ 1 for V
   lds_u8 *dst = T.t == 0 ? R.k + U * C::RAW_BLK : R.v + (U ^ 1) * C::RAW_BLK;
-  if (iss) issue_block<C, PS, FP8>(a, bt, T.g, kb_iss, T.kv_end, T.pg, T.loff, dst);
+  if constexpr (C::SPREAD > 1) {
+    T.kb_iss = iss ? kb_iss : -1;
+    T.dst_iss = dst;
+  }
+  if (iss) {
+    if constexpr (ALL || C::SPREAD == 1)
+      issue_block<C, PS, FP8>(a, bt, T.g, kb_iss, T.kv_end, T.pg, T.loff, dst);
+    else
+      issue_block<C, PS, FP8, 0, C::DPW / C::SPREAD>(a, bt, T.g, kb_iss, T.kv_end, T.pg, T.loff, dst);
+  }
 }
 
 // Step j: K of block j+1 and V of block j are resident after the barrier;
@@ -517,7 +550,7 @@ __device__ __forceinline__ void step(const PrefillArgs &a, const int32_t *bt, Ti
   float ksc[C::NT * 2], vsc[C::NT * 2];
   scale_mask<C, PS, FP8>(a, bt, T, j, s_cur, ksc, vsc);
   // (past the last block this reads a stale K stage; the result is unused)
-  softmax_pv<C, PS, FP8>(a, T, s_cur, ksc, vsc, vb, kb, s_nxt);
+  softmax_pv<C, PS, FP8>(a, bt, T, s_cur, ksc, vsc, vb, kb, s_nxt);
 }
 
 template <int D, int BN, bool FP8, int PS>
@@ -632,7 +665,7 @@ __global__ __launch_bounds__(kThreads, D >= 256 ? 1 : 2) void prefill_kernel(Pre
   T.l = 0.f;
 
   f32x16 sA[C::NT], sB[C::NT];
-  wait_and_issue<C, PS, FP8, 1>(a, bt, T, -1, R);  // U = (-1) & 1
+  wait_and_issue<C, PS, FP8, 1, true>(a, bt, T, -1, R);  // U = (-1) & 1
   {
     const lds_u8 *kb = R.k;
     if constexpr (FP8) {
