@@ -12,7 +12,9 @@
 //     (page, head, first row; scalar arithmetic) plus a per-lane offset
 //     fixed for the whole kernel, which also XOR-swizzles the ring.  One
 //     barrier per block; loads for block j + NS - 1 are issued while block j
-//     is computed.
+//     is computed, in one burst after the barrier (head_dim 256: in three
+//     parts spread over the step, as one wave per SIMD has no partner wave
+//     to cover the burst).
 //   * fp8 pools are loaded raw, then widened to bf16 (exactly) once per
 //     workgroup into a bf16 block with the same layout.
 // Math, per wave of 32 rows:
@@ -158,7 +160,8 @@ __device__ __forceinline__ void block_pages(const int32_t *bt, int kbase, int kv
   }
 }
 
-// Issue this wave's loads of one block of its tensor into a ring stage.  Rows at or beyond
+// Issue this wave's loads [LO, HI) (of DPW) of one block of its tensor into a
+// ring stage; the whole block by default.  Rows at or beyond
 // kv_end (last block only) are redirected to row kv_end - 1: valid, finite
 // data in the same page as the load's first row (or that row's page), which
 // the causal mask removes.
