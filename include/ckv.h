@@ -42,6 +42,9 @@
  *    the host-side bounds max_q_len / max_ctx_len.  Violations are undefined
  *    behaviour (out-of-bounds device accesses); ckv_validate_batch checks
  *    host copies of these arrays.
+ *  - softmax_scale must be positive and finite (the attention calls return
+ *    CKV_ERR_INVALID_ARG otherwise): the kernels remove masked keys with
+ *    -inf scores and fold the scale into the exponent.
  *  - Host-side argument errors return CKV_ERR_INVALID_ARG, combinations
  *    without a kernel return CKV_ERR_UNSUPPORTED, a too-small workspace
  *    returns CKV_ERR_WORKSPACE; nothing is launched in those cases.  A failed
@@ -112,6 +115,12 @@ typedef struct {
 
 /*
  * kv_append -- write the new turn's keys and values into the pool.
+ * Serves Sec. 1 (a tool's output is appended to the request's context and a
+ * new inference step starts) and Sec. 5.2, "Request Pinning" (the finished
+ * step's KV blocks are kept, so the next turn's tokens land in the pages
+ * after the retained prefix).  The paper prints no formula for this write;
+ * it is the paged-pool write of the paged-attention engine it runs on
+ * (Sec. 7).
  * For every sequence b and row t < n_b: position j = ctx_lens[b] + t; for each
  * KV head h, K[page(j)][h][j % page_size][:] = enc(k_new[cu_q_lens[b] + t][h][:]),
  * likewise V.  No other pool byte changes.
@@ -129,6 +138,12 @@ ckv_status_t kv_append(const ckv_pool_t *pool, const ckv_batch_t *batch,
 /*
  * prefix_prefill_attn -- causal attention of the new-turn queries over the
  * retained prefix plus the new turn itself (call kv_append first).
+ * Serves Sec. 1 (the prefill stage: a turn whose prefix was evicted must
+ * recompute it, one whose prefix is retained prefills only its new tokens)
+ * and Sec. 5.2, "Offline Profile" (prefill time against context length,
+ * pages still resident needing no recomputation).  The paper defines no
+ * attention formula; the one below is scaled dot-product softmax attention
+ * with grouped KV heads and a bottom-right causal mask.
  * For row t of sequence b (position i = ctx_lens[b] + t) and query head h:
  *   out[row][h][:] = sum_{j visible} e^{s_j - m} V_j / sum_{j visible} e^{s_j - m},
  *   s_j = softmax_scale * <q[row][h][:], K_j>, m = max_j s_j,
@@ -153,6 +168,9 @@ ckv_status_t prefix_prefill_attn(const ckv_pool_t *pool, const ckv_batch_t *batc
 /*
  * paged_decode_attn -- one query per sequence at position c_b - 1 over its
  * c_b = ctx_lens[b] tokens (its own K/V already appended).  Same formula.
+ * Serves Sec. 1 (the decoding stage, which reads a request's whole KV cache
+ * for every generated token while the cache stays in GPU memory); the
+ * paper gives no formula for it either.
  *   q, out: [num_seqs][num_q_heads][head_dim]; out has q_dtype.
  *   kv_split_len: keys per split-K partition (0 = library choice, else a
  *   positive multiple of 64, at most 256 * page_size).  Partitions are fixed

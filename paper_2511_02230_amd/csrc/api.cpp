@@ -21,6 +21,9 @@ constexpr long long kGridYZ = 65535;
 bool supported_dim(int d) { return d == 64 || d == 128 || d == 256; }
 bool supported_page(int ps) { return ps == 16 || ps == 64; }
 bool valid_dtype(int t) { return t == CKV_F32 || t == CKV_BF16 || t == CKV_FP8_E4M3; }
+// The kernels mask keys with -inf scores and fold the scale into the
+// exponent, which needs a positive, finite softmax scale.
+bool valid_scale(float s) { return std::isfinite(s) && s > 0.f; }
 
 ckv_status_t check_pool(const ckv_pool_t *p) {
   if (!p || !p->k_pages || !p->v_pages) return CKV_ERR_INVALID_ARG;
@@ -159,7 +162,7 @@ ckv_status_t prefix_prefill_attn(const ckv_pool_t *pool, const ckv_batch_t *batc
   CKV_TRY(check_batch(pool, batch, 0));
   CKV_TRY(check_heads(pool, num_q_heads));
   CKV_TRY(check_attn_dtypes(pool, q_dtype));
-  if (!std::isfinite(softmax_scale) || window < 0) return CKV_ERR_INVALID_ARG;
+  if (!valid_scale(softmax_scale) || window < 0) return CKV_ERR_INVALID_ARG;
   if (batch->num_seqs == 0 || batch->total_q_len == 0) return CKV_OK;
   if (!q || !out) return CKV_ERR_INVALID_ARG;
   CKV_TRY(check_prefill_grid(pool, batch, num_q_heads));
@@ -193,7 +196,7 @@ ckv_status_t paged_decode_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
   CKV_TRY(check_batch(pool, batch, 1));
   CKV_TRY(check_heads(pool, num_q_heads));
   CKV_TRY(check_attn_dtypes(pool, q_dtype));
-  if (!std::isfinite(softmax_scale) || window < 0) return CKV_ERR_INVALID_ARG;
+  if (!valid_scale(softmax_scale) || window < 0) return CKV_ERR_INVALID_ARG;
   if (kv_split_len < 0 || kv_split_len % 64 != 0 ||
       kv_split_len > ckv::decode_max_split_len(pool->page_size))
     return CKV_ERR_INVALID_ARG;

@@ -232,17 +232,30 @@ __device__ __forceinline__ void compute_block(const DecodeArgs &a, const DState<
   }
   const float m_use = m == kNegInf ? 0.f : m;
 
-  // ---- P (bf16) and O^T += V^T P^T, one 16-key tile at a time
+  // ---- P (bf16) and O^T += V^T P^T, one 16-key tile at a time.  The row
+  // sum adds the weights the MFMA multiplies: the bf16 probabilities, or for
+  // fp8 the bf16 values of P v_scale divided by v_scale (a value scale of 0,
+  // or one so small or large that P v_scale flushes or overflows, keeps the
+  // fp32 probabilities instead).
 #pragma unroll
   for (int tt = 0; tt < C::NT; ++tt) {
     float p[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      p[j] = fast_exp2(s[tt][j] - m_use);
-      l += p[j];
-      if constexpr (FP8) p[j] *= vsc[tt];
+    for (int j = 0; j < 4; ++j) p[j] = fast_exp2(s[tt][j] - m_use);
+    float praw = 0.f;
+    if constexpr (FP8) {
+      praw = (p[0] + p[1]) + (p[2] + p[3]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) p[j] *= vsc[tt];
     }
     const u32x2 pb = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])};
+    if constexpr (FP8) {
+      const bool vs_ok = (vsc[tt] >= 0x1p-100f) & (vsc[tt] <= 0x1p100f);
+      l = vs_ok ? __builtin_fmaf(add_bf16x2(pb.y, add_bf16x2(pb.x, 0.f)), __builtin_amdgcn_rcpf(vsc[tt]), l)
+                : l + praw;
+    } else {
+      l = add_bf16x2(pb.y, add_bf16x2(pb.x, l));
+    }
     // lane li of group q4 addresses key 4 q4 + li / 4 of the tile, columns
     // 16 dt + 4 (li % 4) .. +3
     const int row = 16 * tt + 4 * q4 + (li >> 2);

@@ -467,7 +467,10 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, const int32_t *
     qk_part<C, 1>(kb_next, T, s_next);
     if (!pos || __builtin_amdgcn_ballot_w64(!(lb <= kSlackSum) | (T.m == kNegInf))) {
       // reduced way: scaled scores (masked ones stay -inf), row maximum,
-      // P = exp2(k_scale scale s - m) v_scale
+      // P = exp2(k_scale scale s - m) v_scale.  The row sum adds the bf16
+      // values of P v_scale divided by v_scale, the weights the MFMA
+      // multiplies, unless the value scale is outside 2^-100 .. 2^100 (0 for
+      // a page of zeros): then the fp32 probabilities
 #pragma unroll
       for (int q = 0; q < C::NT * 2; ++q)
 #pragma unroll
@@ -480,15 +483,21 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, const int32_t *
       lb = 0.f;
 #pragma unroll
       for (int q = 0; q < C::NT * 2; ++q) {
-        float p[8];
+        float p[8], praw = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           p[e] = fast_exp2(s[q >> 1][8 * (q & 1) + e] - m_use);
-          lb += p[e];
+          praw += p[e];
           p[e] *= vsc[q];
         }
         pb[q] = u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
                       pack_bf16x2(p[6], p[7])};
+        float ss = add_bf16x2(pb[q].x, 0.f);
+        ss = add_bf16x2(pb[q].y, ss);
+        ss = add_bf16x2(pb[q].z, ss);
+        ss = add_bf16x2(pb[q].w, ss);
+        const bool vs_ok = (vsc[q] >= 0x1p-100f) & (vsc[q] <= 0x1p100f);
+        lb = vs_ok ? __builtin_fmaf(ss, ivs[q], lb) : lb + praw;
       }
     }
     T.l += lb;

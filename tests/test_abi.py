@@ -89,11 +89,16 @@ def test_attention_argument_checks(ckv):
     assert f(ctypes.byref(P), ctypes.byref(B), 1, 1, 3, 0.1, 0, 1, None, 0, None) == 1  # 3 % 2
     assert f(ctypes.byref(P), ctypes.byref(B), 1, 0, 4, 0.1, 0, 1, None, 0, None) == 2  # f32 q, bf16 pool
     assert f(ctypes.byref(P), ctypes.byref(B), 1, 1, 4, float("nan"), 0, 1, None, 0, None) == 1
+    # the softmax scale must be positive: the kernels mask with -inf scores
+    for bad_scale in (0.0, -0.0, -0.1, float("inf")):
+        assert f(ctypes.byref(P), ctypes.byref(B), 1, 1, 4, bad_scale, 0, 1, None, 0, None) == 1
     assert f(ctypes.byref(P), ctypes.byref(B), 1, 1, 4, 0.1, -1, 1, None, 0, None) == 1
     assert f(ctypes.byref(P), ctypes.byref(B), None, 1, 4, 0.1, 0, 1, None, 0, None) == 1
     d = ckv.LIB.paged_decode_attn
     DB = _batch(ckv, cu_q_lens=None, max_ctx_len=20000, max_pages_per_seq=2000)
     assert d(ctypes.byref(P), ctypes.byref(DB), 1, 1, 4, 0.1, 0, 100, 1, None, 0, None) == 1  # split % 64
+    for bad_scale in (0.0, -1.0):
+        assert d(ctypes.byref(P), ctypes.byref(DB), 1, 1, 4, bad_scale, 0, 0, 1, None, 0, None) == 1
     need = ckv.LIB.paged_decode_workspace_bytes(ctypes.byref(P), ctypes.byref(DB), 4, 0)
     assert need > 0
     assert d(ctypes.byref(P), ctypes.byref(DB), 1, 1, 4, 0.1, 0, 0, 1, None, 0, None) == 3

@@ -6,7 +6,10 @@ on seeded synthetic inputs and compares with the oracle on the same inputs:
                        stay poisoned)
   attention, f32       max |err| <= 1e-5
   attention, bf16      max |err| <= 2e-2 and mean |err| <= 2e-3
-  attention, fp8 KV    max |err| <= 3e-2
+  attention, fp8 KV    max |err| <= 3e-2 and mean |err| <= 2e-3
+and, for bf16 and fp8, every output row within 2 % (mean |err|) of the
+oracle row's RMS and 10 % (max |err|) of its largest value, which keeps
+the check able to fail at long context (tests/parity.py).
 Small cases compare every output; the full-size configurations (in the
 launch configuration the benchmark times) compare sampled sequences / rows.
 """
@@ -19,11 +22,10 @@ import torch
 
 import workload
 from oracle import formats
+from tests import parity
 from tests.oracle_inputs import OracleState, to_numpy
 
 pytestmark = pytest.mark.gpu
-
-TOL = {"f32": (1e-5, None), "bf16": (2e-2, 2e-3), "fp8": (3e-2, 2e-3)}
 
 
 def say(*a):
@@ -37,24 +39,15 @@ def _gpu():
     from paper_2511_02230_amd import ckv  # noqa: F401  (fails loudly if libckv.so is missing)
 
 
-def tol_of(cfg):
-    return TOL["fp8" if cfg.kv_dtype == "fp8" else cfg.q_dtype]
-
-
 def out_f64(t):
     x = to_numpy(t)
     return formats.bf16_bits_to_f64(x) if x.dtype == np.uint16 else x.astype(np.float64)
 
 
 def check_close(got, ref, cfg, what):
-    mx_tol, mean_tol = tol_of(cfg)
-    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
-    err = np.abs(got - ref)
-    mx, mean = float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
-    say(f"  {what}: max {mx:.3e} mean {mean:.3e}")
-    assert mx <= mx_tol, f"{what}: max abs err {mx} > {mx_tol}"
-    if mean_tol is not None:
-        assert mean <= mean_tol, f"{what}: mean abs err {mean} > {mean_tol}"
+    bad, summary = parity.failures(got, ref, parity.kind_of(cfg))
+    say(f"  {what}: {summary}")
+    assert not bad, f"{what}: " + "; ".join(bad)
 
 
 def check_pool(dw, st, what):
@@ -230,13 +223,18 @@ def test_page_shuffle_is_bit_identical(kv):
 
 
 def test_decode_matches_one_row_prefill_on_gpu():
+    """decode(c) and a one-row prefill at P = c - 1 give the same row: each
+    within the bars of the oracle, and the two within the per-row bar of
+    each other."""
     from paper_2511_02230_amd import ckv
     from paper_2511_02230_amd.harness import DeviceWorkload
 
     cfg = cfg_of("dvp", 32, 8, 128, 16, "bf16")
-    wl = workload.make_workload(cfg, prefill=[], decode=[1000, 77, 4096])
+    wl = workload.make_workload(cfg, prefill=[], decode=[1000, 77, 4096, 20000])
     dw = DeviceWorkload(wl, "cuda")
+    st = OracleState(wl, device="cuda")
     dw.append_decode()
+    st.append_decode()
     dec = out_f64(dw.run_decode())
     dcx = wl.decode_ctx
     # the same queries as one-row prefills at P = c - 1
@@ -245,7 +243,100 @@ def test_decode_matches_one_row_prefill_on_gpu():
     cu = torch.arange(len(dcx) + 1, dtype=torch.int32, device="cuda")
     batch = ckv.Batch(bt, ctx, cu, len(dcx), 1, int(dcx.max()) - 1)
     pre = out_f64(ckv.prefix_prefill_attn(dw.pool, batch, dw.q_decode, cfg.softmax_scale))
-    assert np.max(np.abs(dec - pre)) <= 2e-2
+    ref = st.decode(to_numpy(dw.q_decode), st.rows_of(wl.decode))
+    for b, r in ref.items():
+        check_close(dec[b], r, cfg, f"decode c={dcx[b]}")
+        check_close(pre[b], r, cfg, f"one-row prefill P={dcx[b] - 1}")
+        check_close(dec[b], pre[b], cfg, f"decode vs one-row prefill c={dcx[b]}")
+
+
+def _plant_keys(dw, st, sid, upto, rng, every=2048):
+    """In each `every`-key range of sequence `sid` below position `upto`,
+    overwrite one key (all KV heads) with a large component on dimension 0
+    and its value with a one-hot on dimension r (the range's index), in the
+    GPU pool and the oracle's pool alike.  fp8 pages are re-encoded around
+    the planted row with a new (page, head) scale.  Returns the planted
+    positions."""
+    cfg, wl = dw.cfg, dw.wl
+    ps, D = cfg.page_size, cfg.head_dim
+    seq = wl.seqs[sid]
+    planted = []
+    for r, r0 in enumerate(range(0, upto, every)):
+        j = r0 + int(rng.integers(0, min(every, upto - r0)))
+        planted.append(j)
+        page = int(seq.pages[j // ps])
+        comp = int(st.page_map[page])
+        slot = j % ps
+        kvec = np.zeros(D, np.float32)
+        kvec[0] = 16.0
+        vvec = np.zeros(D, np.float32)
+        vvec[r % D] = 1.0
+        for name, vec in (("k", kvec), ("v", vvec)):
+            host = getattr(st, f"pool_{name}")
+            if cfg.kv_dtype == "fp8":
+                scale = getattr(st, f"{name}_scale")
+                valid = np.arange(ps) + (j // ps) * ps < seq.length
+                for g in range(cfg.num_kv_heads):
+                    vals = formats.e4m3_to_f64(host[comp, g]) * np.float64(scale[comp, g])
+                    vals[slot] = vec
+                    vals = vals[valid].astype(np.float32)
+                    sc = np.float32(np.abs(vals).max() / 448.0)
+                    host[comp, g, valid] = formats.fp8_quantize(vals, sc)
+                    scale[comp, g] = sc
+                gpu_scale = getattr(dw.pool, f"{name}_scale")
+                gpu_scale[page] = torch.as_tensor(scale[comp], device="cuda")
+                getattr(dw.pool, name)[page] = torch.as_tensor(host[comp], device="cuda")
+            else:
+                bits = formats.bf16_bits_from_f32(vec)
+                host[comp, :, slot, :] = bits
+                getattr(dw.pool, name)[page, :, slot, :] = (
+                    torch.from_numpy(bits.view(np.int16)).to("cuda").view(torch.bfloat16))
+    torch.cuda.synchronize()
+    return planted
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+def test_every_key_partition_carries_weight(kv):
+    """Long prefixes cut into many key partitions (prefill: 20 of 2048 keys
+    for bf16, 32 of 2240 for fp8; decode: the library's split and 2048),
+    with one planted key per 2048-key range whose score (~11 in natural
+    units, against ~5 for the largest of the others) gives it ~5 % of the
+    weight: each range adds ~0.05 on its own output dimension, so a lost
+    partition, block or merge weight breaks even the absolute bounds."""
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    if kv == "bf16":
+        cfg, P, n = cfg_of("plant16", 8, 1, 128, 16, "bf16"), 40000, 64
+    else:
+        cfg, P, n = cfg_of("plant8", 16, 2, 128, 64, "fp8"), 70000, 32
+    wl = workload.make_workload(cfg, prefill=[(P, n)], decode=[P + n])
+    say(f"case planted keys kv={kv} P={P} n={n}")
+    dw = DeviceWorkload(wl, "cuda")
+    st = OracleState(wl, device="cuda")
+    dw.append_prefill()
+    dw.append_decode()
+    torch.cuda.synchronize()
+    st.append_prefill()
+    st.append_decode()
+    rng = np.random.default_rng([P, 17])
+    planted = []
+    for sid in range(len(wl.seqs)):
+        planted = _plant_keys(dw, st, sid, P, rng)
+    dw.q_prefill[..., 0] = 8.0
+    dw.q_decode[..., 0] = 8.0
+    torch.cuda.synchronize()
+    nr = len(planted)
+    pf, dc = wl.prefill, wl.decode
+    ref = st.prefill(to_numpy(dw.q_prefill), st.rows_of(pf))[0]
+    # every range carries weight in the oracle's output
+    assert float(ref[..., :nr].min()) > 0.02, float(ref[..., :nr].min())
+    got = out_f64(dw.run_prefill())
+    check_close(got, ref, cfg, f"prefill P={P} n={n}, {nr} planted keys")
+    ref_d = st.decode(to_numpy(dw.q_decode), st.rows_of(dc))[0]
+    assert float(ref_d[..., :nr].min()) > 0.02
+    for split in (0, 2048):
+        got = out_f64(dw.run_decode(kv_split_len=split))
+        check_close(got[0], ref_d, cfg, f"decode c={P + n} split {split}")
 
 
 def test_fp8_quantizer_every_bf16_value():
