@@ -184,6 +184,31 @@ ckv_status_t paged_decode_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
                                void *out, void *workspace, size_t workspace_bytes,
                                hipStream_t stream);
 
+/*
+ * paged_decode_attn_noalloc -- paged_decode_attn without a workspace, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).  Same arguments,
+ * kernels and results as paged_decode_attn (bit for bit, for the same
+ * kv_split_len), minus workspace / workspace_bytes: the split-K partials go
+ * to a scratch array of CKV_DECODE_SCRATCH_BYTES bytes that the library
+ * keeps in each GPU's memory from its first use on that GPU until the
+ * process ends (the stream must belong to the current device).  The call
+ * allocates and frees nothing.
+ *   Returns CKV_ERR_WORKSPACE, launching nothing, when the partials would
+ *   exceed the scratch (paged_decode_workspace_bytes(...) >
+ *   CKV_DECODE_SCRATCH_BYTES); a longer kv_split_len needs fewer of them.
+ *   CKV_ERR_LAUNCH if the scratch address cannot be obtained.
+ *   Every call on one GPU shares that GPU's scratch: calls whose work
+ *   overlaps on the GPU (concurrent streams, or threads) race and must be
+ *   serialized by the caller.  A call needs no cleared scratch: each
+ *   partition writes its partial before the merge reads it.
+ */
+#define CKV_DECODE_SCRATCH_BYTES ((size_t)64 << 20)
+ckv_status_t paged_decode_attn_noalloc(const ckv_pool_t *pool, const ckv_batch_t *batch,
+                                       const void *q, ckv_dtype_t q_dtype, int32_t num_q_heads,
+                                       float softmax_scale, int32_t window, int32_t kv_split_len,
+                                       void *out, hipStream_t stream);
+
 /* Workspace sizes in bytes for the calls above (0 when none is needed).
  * Return 0 as well for invalid arguments, which the calls then reject. */
 size_t prefix_prefill_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t *batch,

@@ -22,7 +22,8 @@ LIB_PATH = os.path.join(_PKG, "libckv.so")
 CKV_F32, CKV_BF16, CKV_FP8_E4M3 = 0, 1, 2
 STATUS = {0: "CKV_OK", 1: "CKV_ERR_INVALID_ARG", 2: "CKV_ERR_UNSUPPORTED", 3: "CKV_ERR_WORKSPACE",
           4: "CKV_ERR_LAUNCH"}
-EXPORTS = ("kv_append", "prefix_prefill_attn", "paged_decode_attn", "prefix_prefill_workspace_bytes",
+EXPORTS = ("kv_append", "prefix_prefill_attn", "paged_decode_attn", "paged_decode_attn_noalloc",
+           "prefix_prefill_workspace_bytes",
            "paged_decode_workspace_bytes", "kv_pages_reload", "kv_pages_offload",
            "kv_pages_staging_bytes", "ckv_validate_batch", "ckv_status_string", "ckv_version")
 
@@ -58,6 +59,7 @@ def _load():
         "kv_append": ([P, B, vp, vp, ctypes.c_int, vp], ctypes.c_int),
         "prefix_prefill_attn": ([P, B, vp, ctypes.c_int, i32, f32, i32, vp, vp, sz, vp], ctypes.c_int),
         "paged_decode_attn": ([P, B, vp, ctypes.c_int, i32, f32, i32, i32, vp, vp, sz, vp], ctypes.c_int),
+        "paged_decode_attn_noalloc": ([P, B, vp, ctypes.c_int, i32, f32, i32, i32, vp, vp], ctypes.c_int),
         "prefix_prefill_workspace_bytes": ([P, B, i32], sz),
         "paged_decode_workspace_bytes": ([P, B, i32, i32], sz),
         "kv_pages_reload": ([P, vp, i32, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
@@ -238,6 +240,27 @@ def paged_decode_attn(pool: Pool, batch: Batch, q: torch.Tensor, softmax_scale: 
         ctypes.byref(pc), ctypes.byref(bc), _ptr(q), _Q_DTYPES[q.dtype], q.shape[1],
         float(softmax_scale), int(window), int(kv_split_len), _ptr(out), _ptr(ws), wsb,
         _stream(stream)))
+    return out
+
+
+DECODE_SCRATCH_BYTES = 64 << 20  # CKV_DECODE_SCRATCH_BYTES
+
+
+def paged_decode_attn_noalloc(pool: Pool, batch: Batch, q: torch.Tensor, softmax_scale: float,
+                              out: torch.Tensor, window: int = 0, kv_split_len: int = 0,
+                              stream=None) -> torch.Tensor:
+    """paged_decode_attn with its partials in the library's per-GPU scratch:
+    nothing is allocated (out must be given)."""
+    _dev(q, "q")
+    if q.dtype not in _Q_DTYPES or q.dim() != 3 or q.shape[0] != batch.num_seqs:
+        raise ValueError("q must be [num_seqs, H_q, D] float32 or bfloat16")
+    _dev(out, "out", q.dtype)
+    if out.shape != q.shape:
+        raise ValueError("out must have q's shape")
+    pc, bc = pool.c(), batch.c()
+    _check("paged_decode_attn_noalloc", LIB.paged_decode_attn_noalloc(
+        ctypes.byref(pc), ctypes.byref(bc), _ptr(q), _Q_DTYPES[q.dtype], q.shape[1],
+        float(softmax_scale), int(window), int(kv_split_len), _ptr(out), _stream(stream)))
     return out
 
 

@@ -213,6 +213,32 @@ ckv_status_t paged_decode_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
                                           stream));
 }
 
+ckv_status_t paged_decode_attn_noalloc(const ckv_pool_t *pool, const ckv_batch_t *batch,
+                                       const void *q, ckv_dtype_t q_dtype, int32_t num_q_heads,
+                                       float softmax_scale, int32_t window, int32_t kv_split_len,
+                                       void *out, hipStream_t stream) {
+  CKV_TRY(check_pool(pool));
+  CKV_TRY(check_batch(pool, batch, 1));
+  CKV_TRY(check_heads(pool, num_q_heads));
+  CKV_TRY(check_attn_dtypes(pool, q_dtype));
+  if (!valid_scale(softmax_scale) || window < 0) return CKV_ERR_INVALID_ARG;
+  if (kv_split_len < 0 || kv_split_len % 64 != 0 ||
+      kv_split_len > ckv::decode_max_split_len(pool->page_size))
+    return CKV_ERR_INVALID_ARG;
+  if (batch->num_seqs == 0) return CKV_OK;
+  if (!q || !out) return CKV_ERR_INVALID_ARG;
+  if (q_dtype == CKV_F32)  // the fp32 path keeps no partials
+    return launched(ckv::launch_attn_f32(view(pool), view(batch), static_cast<const float *>(q),
+                                         num_q_heads, softmax_scale, window, true,
+                                         static_cast<float *>(out), stream));
+  const size_t need = ckv::decode_workspace_bytes(view(pool), view(batch), num_q_heads, kv_split_len);
+  if (need > CKV_DECODE_SCRATCH_BYTES) return CKV_ERR_WORKSPACE;
+  void *ws = nullptr;
+  if (need > 0 && ckv::decode_scratch(&ws) != hipSuccess) return CKV_ERR_LAUNCH;
+  return launched(ckv::launch_decode_bf16(view(pool), view(batch), q, num_q_heads, softmax_scale,
+                                          window, kv_split_len, out, ws, need, stream));
+}
+
 size_t kv_pages_staging_bytes(const ckv_pool_t *pool, int32_t num_moved) {
   if (check_pool(pool) != CKV_OK || num_moved <= 0) return 0;
   return ckv::pages_staging_bytes(view(pool), num_moved);

@@ -29,7 +29,9 @@
 // only one, in which case it writes the output; the combine kernel merges
 // the rest.
 #include <algorithm>
+#include <mutex>
 
+#include "../../include/ckv.h"
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -518,6 +520,38 @@ hipError_t launch_decode_bf16(const PoolView &p, const BatchView &b, const void 
       return fp8 ? launch<256, true>(a, p.ps, b.num_seqs, s) : launch<256, false>(a, p.ps, b.num_seqs, s);
   }
   return hipErrorInvalidValue;
+}
+
+// ------------------------------------------------- allocation-free decode
+// The split-K partials of paged_decode_attn_noalloc live in this file-scope
+// device array instead of a caller workspace.  Each GPU the library runs on
+// holds its own copy until the process ends; every call on a GPU shares it.
+// On the host, `scratch` names a host-side stand-in, never the device copy:
+// host code uses only the device address that hipGetSymbolAddress returns,
+// looked up once per device (with that device current) and kept here.
+namespace {
+__device__ __align__(256) uint8_t scratch[CKV_DECODE_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void *scratch_dev[kMaxDevices];  // device address of `scratch` per device
+}  // namespace
+
+hipError_t decode_scratch(void **ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_dev[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    scratch_dev[dev] = p;
+  }
+  *ptr = scratch_dev[dev];
+  return hipSuccess;
 }
 
 }  // namespace ckv

@@ -38,6 +38,10 @@ hipError_t launch_decode_bf16(const PoolView &p, const BatchView &b, const void 
                               float scale, int window, int split_len, void *out, void *ws,
                               size_t ws_bytes, hipStream_t s);
 
+// Device address of the allocation-free decode's scratch on the current
+// device (CKV_DECODE_SCRATCH_BYTES bytes), looked up on first use.
+hipError_t decode_scratch(void **ptr);
+
 int page_bytes(const PoolView &p);
 int page_blocks(const PoolView &p);
 size_t pages_staging_bytes(const PoolView &p, int n);

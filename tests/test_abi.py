@@ -174,3 +174,20 @@ def test_prefill_key_partitions(ckv, h_q, h_kv, d, n, prefix, splits):
     B = _batch(ckv, max_pages_per_seq=pages, total_q_len=n, max_q_len=n, max_ctx_len=prefix)
     got = ckv.LIB.prefix_prefill_workspace_bytes(ctypes.byref(P), ctypes.byref(B), h_q)
     assert got == (0 if splits == 1 else n * h_q * splits * (d + 2) * 4)
+
+
+def test_noalloc_decode_checks_arguments_and_the_scratch_bound_on_the_host(ckv):
+    """paged_decode_attn_noalloc rejects what paged_decode_attn rejects, and
+    partials larger than its scratch, before touching the GPU."""
+    P = _pool(ckv, num_pages=100000)
+    f = ckv.LIB.paged_decode_attn_noalloc
+    DB = _batch(ckv, cu_q_lens=None, max_ctx_len=20000, max_pages_per_seq=2000)
+    assert f(ctypes.byref(P), ctypes.byref(DB), 1, 1, 3, 0.1, 0, 0, 1, None) == 1  # 3 % 2
+    assert f(ctypes.byref(P), ctypes.byref(DB), 1, 1, 4, 0.0, 0, 0, 1, None) == 1  # scale
+    assert f(ctypes.byref(P), ctypes.byref(DB), 1, 1, 4, 0.1, 0, 100, 1, None) == 1  # split % 64
+    assert f(ctypes.byref(P), ctypes.byref(DB), 1, 1, 4, 0.1, 0, 0, None, None) == 1  # no out
+    assert f(ctypes.byref(P), ctypes.byref(_batch(ckv, num_seqs=0)), 1, 1, 4, 0.1, 0, 0, 1, None) == 0
+    big = _batch(ckv, num_seqs=4096, cu_q_lens=None, max_ctx_len=65536, max_pages_per_seq=4096)
+    need = ckv.LIB.paged_decode_workspace_bytes(ctypes.byref(P), ctypes.byref(big), 64, 512)
+    assert need > ckv.DECODE_SCRATCH_BYTES
+    assert f(ctypes.byref(P), ctypes.byref(big), 1, 1, 64, 0.1, 0, 512, 1, None) == 3
