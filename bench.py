@@ -8,6 +8,10 @@ turns; a 128-sequence decode batch):
     kv_append(new turn) -> prefix_prefill_attn -> kv_append(decode token)
     -> paged_decode_attn
 
+and the same step as one mixed launch (both appends, then mixed_attn: the
+prefill's row tiles and the decode's partitions in one grid) is timed after
+it and reported as "mixed_step".
+
 Inputs are synthetic and already resident in HBM when timing starts.  The
 headline value is prefix_prefill_attn's throughput in algorithmic TFLOP/s
 (4 * D * H_q per visible (query row, key) pair); the decode kernel's
@@ -181,6 +185,37 @@ def main():
     per = {nm: float(np.mean([ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(args.steps)]))
            for i, nm in enumerate(names)}
 
+    # the same step as one mixed launch: both appends, then prefill and decode
+    # work items in one grid (decode partitions of the mixed launch's own
+    # length), timed the same way
+    from paper_2511_02230_amd import ckv
+
+    mixed = None
+    if cfg.q_dtype == "bf16" and wl.prefill.num_seqs and wl.decode.num_seqs:
+        mws_n = ckv.mixed_workspace_bytes(dw.pool, dw.prefill, dw.decode, cfg.num_q_heads)
+        mws = torch.empty(max(1, mws_n), dtype=torch.uint8, device="cuda")
+        op, od = torch.empty_like(dw.out_prefill), torch.empty_like(dw.out_decode)
+
+        def mixed_step():
+            dw.append_prefill()
+            dw.append_decode()
+            ckv.mixed_attn(dw.pool, dw.prefill, dw.q_prefill, dw.decode, dw.q_decode, cfg.softmax_scale,
+                           args.window, out_prefill=op, out_decode=od, workspace=mws)
+
+        for _ in range(args.warmup):
+            mixed_step()
+        torch.cuda.synchronize()
+        m0 = torch.cuda.Event(enable_timing=True)
+        m1 = torch.cuda.Event(enable_timing=True)
+        m0.record(stream)
+        for _ in range(args.steps):
+            mixed_step()
+        m1.record(stream)
+        torch.cuda.synchronize()
+        mixed_ms = m0.elapsed_time(m1) / args.steps
+        mixed = {"ms_per_step": mixed_ms, "sequential_ms_per_step": ms_step, "speedup": ms_step / mixed_ms,
+                 "launch": "kv_append x2 + mixed_attn (prefill row tiles and decode partitions in one grid)"}
+
     w = args.window
     # the stored traffic was measured on the default workload only
     default_cfg = args.config == "llama3.1-70b" and w == 0
@@ -240,6 +275,7 @@ def main():
         "roofline": rooflines["prefix_prefill_attn"],
         "rooflines": rooflines,
         "cpu_baseline": cpu,
+        "mixed_step": mixed,
     }
     print(json.dumps(line), flush=True)
 

@@ -185,6 +185,44 @@ ckv_status_t paged_decode_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
                                hipStream_t stream);
 
 /*
+ * mixed_attn -- prefix_prefill_attn over `prefill` and paged_decode_attn over
+ * `decode` in one kernel launch (followed by the small merges of split keys
+ * when either needs them), for a serving step whose batch mixes
+ * prefix-reuse prefills with decodes: the paper's engine runs such steps
+ * with chunked prefill (Sec. 6.1, "Setup"), and the time a turn spends in
+ * prefill is the cost its TTL weighs (Sec. 4.1; Sec. 5.2, "Offline
+ * Profile").  The prefill's work is bound by the matrix cores and the
+ * decode's by HBM; one grid holding both lets decode partitions stream
+ * beside prefill row tiles.
+ * Results are those of the two separate calls, bit for bit (same work
+ * items, same key partitions), with the same argument rules; `prefill`
+ * follows prefix_prefill_attn's batch conventions and `decode`
+ * paged_decode_attn's.  Both read the pool only: append both batches' new
+ * K/V first.  Either batch may be empty (num_seqs 0).
+ *   q_dtype: CKV_BF16 (bf16 or fp8 pools); other types return
+ *   CKV_ERR_UNSUPPORTED.
+ *   kv_split_len: the decode's partition length, as for paged_decode_attn;
+ *   0 = paged_decode_attn's own choice capped at 2048 keys (finer decode
+ *   work interleaves better with the prefill's), so the decode output
+ *   equals paged_decode_attn's at that length.
+ *   interleave: the grid alternates runs of `interleave` groups of eight
+ *   prefill workgroups with runs of as many decode groups (0 = the library's
+ *   choice: three fills of the GPU).  It changes timing only, never
+ *   results; negative values return CKV_ERR_INVALID_ARG.
+ *   workspace: at least mixed_attn_workspace_bytes(...) bytes, 256-byte
+ *   aligned (the prefill's partials, then the decode's).
+ */
+ckv_status_t mixed_attn(const ckv_pool_t *pool, const ckv_batch_t *prefill, const void *q_prefill,
+                        void *out_prefill, const ckv_batch_t *decode, const void *q_decode,
+                        void *out_decode, ckv_dtype_t q_dtype, int32_t num_q_heads,
+                        float softmax_scale, int32_t window, int32_t kv_split_len,
+                        int32_t interleave, void *workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+size_t mixed_attn_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t *prefill,
+                                  const ckv_batch_t *decode, int32_t num_q_heads,
+                                  int32_t kv_split_len);
+
+/*
  * paged_decode_attn_noalloc -- paged_decode_attn without a workspace, for
  * callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid hipMalloc).  Same arguments,

@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libckv.so")
 
-SOURCES = ["api.cpp", "kv_append.hip", "attn_f32.hip", "prefill_bf16.hip", "decode_bf16.hip", "kv_pages.hip", "ttl.cpp"]
+SOURCES = ["api.cpp", "kv_append.hip", "attn_f32.hip", "prefill_bf16.hip", "decode_bf16.hip", "mixed.hip", "kv_pages.hip", "ttl.cpp"]
 ARCH = "gfx950"
 
 

@@ -23,7 +23,7 @@ CKV_F32, CKV_BF16, CKV_FP8_E4M3 = 0, 1, 2
 STATUS = {0: "CKV_OK", 1: "CKV_ERR_INVALID_ARG", 2: "CKV_ERR_UNSUPPORTED", 3: "CKV_ERR_WORKSPACE",
           4: "CKV_ERR_LAUNCH"}
 EXPORTS = ("kv_append", "prefix_prefill_attn", "paged_decode_attn", "paged_decode_attn_noalloc",
-           "prefix_prefill_workspace_bytes",
+           "mixed_attn", "mixed_attn_workspace_bytes", "prefix_prefill_workspace_bytes",
            "paged_decode_workspace_bytes", "kv_pages_reload", "kv_pages_offload",
            "kv_pages_staging_bytes", "ckv_validate_batch", "ckv_status_string", "ckv_version")
 
@@ -60,6 +60,9 @@ def _load():
         "prefix_prefill_attn": ([P, B, vp, ctypes.c_int, i32, f32, i32, vp, vp, sz, vp], ctypes.c_int),
         "paged_decode_attn": ([P, B, vp, ctypes.c_int, i32, f32, i32, i32, vp, vp, sz, vp], ctypes.c_int),
         "paged_decode_attn_noalloc": ([P, B, vp, ctypes.c_int, i32, f32, i32, i32, vp, vp], ctypes.c_int),
+        "mixed_attn": ([P, B, vp, vp, B, vp, vp, ctypes.c_int, i32, f32, i32, i32, i32, vp, sz, vp],
+                       ctypes.c_int),
+        "mixed_attn_workspace_bytes": ([P, B, B, i32, i32], sz),
         "prefix_prefill_workspace_bytes": ([P, B, i32], sz),
         "paged_decode_workspace_bytes": ([P, B, i32, i32], sz),
         "kv_pages_reload": ([P, vp, i32, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
@@ -241,6 +244,38 @@ def paged_decode_attn(pool: Pool, batch: Batch, q: torch.Tensor, softmax_scale: 
         float(softmax_scale), int(window), int(kv_split_len), _ptr(out), _ptr(ws), wsb,
         _stream(stream)))
     return out
+
+
+def mixed_workspace_bytes(pool: Pool, prefill: Batch, decode: Batch, num_q_heads: int,
+                          kv_split_len: int = 0) -> int:
+    pc, pb, db = pool.c(), prefill.c(), decode.c()
+    return int(LIB.mixed_attn_workspace_bytes(ctypes.byref(pc), ctypes.byref(pb), ctypes.byref(db),
+                                              num_q_heads, kv_split_len))
+
+
+def mixed_attn(pool: Pool, prefill: Batch, q_prefill: torch.Tensor, decode: Batch, q_decode: torch.Tensor,
+               softmax_scale: float, window: int = 0, kv_split_len: int = 0, interleave: int = 0,
+               out_prefill=None, out_decode=None, workspace=None, stream=None):
+    """Prefill over `prefill` (q_prefill [total_q_len, H_q, D]) and decode over
+    `decode` (q_decode [num_seqs, H_q, D]) in one launch; returns
+    (out_prefill, out_decode)."""
+    _dev(q_prefill, "q_prefill", torch.bfloat16)
+    _dev(q_decode, "q_decode", torch.bfloat16)
+    if q_prefill.dim() != 3 or q_prefill.shape[0] != prefill.total_q_len:
+        raise ValueError("q_prefill must be [total_q_len, H_q, D]")
+    if q_decode.dim() != 3 or q_decode.shape[0] != decode.num_seqs or q_decode.shape[1:] != q_prefill.shape[1:]:
+        raise ValueError("q_decode must be [num_seqs, H_q, D]")
+    out_prefill = _out_like(q_prefill, out_prefill)
+    out_decode = _out_like(q_decode, out_decode)
+    h_q = q_prefill.shape[1]
+    ws, wsb = _workspace(mixed_workspace_bytes(pool, prefill, decode, h_q, kv_split_len), workspace,
+                         q_prefill.device)
+    pc, pb, db = pool.c(), prefill.c(), decode.c()
+    _check("mixed_attn", LIB.mixed_attn(
+        ctypes.byref(pc), ctypes.byref(pb), _ptr(q_prefill), _ptr(out_prefill), ctypes.byref(db),
+        _ptr(q_decode), _ptr(out_decode), CKV_BF16, h_q, float(softmax_scale), int(window),
+        int(kv_split_len), int(interleave), _ptr(ws), wsb, _stream(stream)))
+    return out_prefill, out_decode
 
 
 DECODE_SCRATCH_BYTES = 64 << 20  # CKV_DECODE_SCRATCH_BYTES

@@ -38,6 +38,18 @@ hipError_t launch_decode_bf16(const PoolView &p, const BatchView &b, const void 
                               float scale, int window, int split_len, void *out, void *ws,
                               size_t ws_bytes, hipStream_t s);
 
+// Prefill over one batch and decode over another in one launch (plus the
+// merges of split keys); results equal the two separate launches bit for bit
+// at the same decode partition length (mixed_split_len resolves 0).
+// interleave: groups of eight workgroups per run of one kind (0 = library
+// choice).
+int mixed_split_len(const PoolView &p, const BatchView &db, int h_q, int requested);
+size_t mixed_workspace_bytes(const PoolView &p, const BatchView &pb, const BatchView &db, int h_q,
+                             int split_len);
+hipError_t launch_mixed(const PoolView &p, const BatchView &pb, const void *q_pf, void *out_pf,
+                        const BatchView &db, const void *q_dc, void *out_dc, int h_q, float scale,
+                        int window, int split_len, int interleave, void *ws, hipStream_t s);
+
 // Device address of the allocation-free decode's scratch on the current
 // device (CKV_DECODE_SCRATCH_BYTES bytes), looked up on first use.
 hipError_t decode_scratch(void **ptr);

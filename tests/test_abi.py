@@ -191,3 +191,32 @@ def test_noalloc_decode_checks_arguments_and_the_scratch_bound_on_the_host(ckv):
     need = ckv.LIB.paged_decode_workspace_bytes(ctypes.byref(P), ctypes.byref(big), 64, 512)
     assert need > ckv.DECODE_SCRATCH_BYTES
     assert f(ctypes.byref(P), ctypes.byref(big), 1, 1, 64, 0.1, 0, 512, 1, None) == 3
+
+
+def test_mixed_launch_checks_arguments_on_the_host(ckv):
+    """mixed_attn applies both calls' checks before launching anything."""
+    P = _pool(ckv, num_pages=100000)
+    f = ckv.LIB.mixed_attn
+    PB = _batch(ckv)
+    DB = _batch(ckv, cu_q_lens=None, max_ctx_len=2000, max_pages_per_seq=200)
+    E = _batch(ckv, num_seqs=0)
+
+    def call(pb=PB, db=DB, qp=1, op=1, qd=1, od=1, qdt=1, hq=4, scale=0.1, w=0, split=0, inter=0,
+             ws=1, wsb=1 << 30):
+        return f(ctypes.byref(P), ctypes.byref(pb), qp, op, ctypes.byref(db), qd, od, qdt, hq, scale, w,
+                 split, inter, ws, wsb, None)
+
+    assert call(hq=3) == 1                 # 3 % 2
+    assert call(qdt=0) == 2                # fp32 queries: no mixed kernel
+    assert call(scale=0.0) == 1
+    assert call(w=-1) == 1
+    assert call(split=100) == 1            # not a multiple of 64
+    assert call(inter=-1) == 1
+    assert call(qp=None) == 1              # prefill rows without queries
+    assert call(od=None) == 1              # decode rows without an output
+    assert call(pb=E, db=E) == 0           # nothing to do
+    need = ckv.LIB.mixed_attn_workspace_bytes(ctypes.byref(P), ctypes.byref(PB), ctypes.byref(DB), 4, 128)
+    assert need > 0
+    assert call(split=128, ws=None) == 3
+    assert call(split=128, wsb=need - 1) == 3
+    assert call(split=128, ws=1 << 20 | 16) == 1   # not 256-byte aligned

@@ -512,3 +512,113 @@ def test_empty_and_degenerate_batches():
                   torch.zeros((0, 2, 128), dtype=torch.bfloat16, device="cuda"))
     ckv.prefix_prefill_attn(dw_pool, empty, q, 0.1)
     torch.cuda.synchronize()
+
+
+# ------------------------------------------------- mixed prefill + decode
+
+MIXED = [
+    (cfg_of("m1", 32, 8, 128, 16, "bf16"), [(300, 70), (0, 200), (1000, 33)], [1, 700, 2049, 64], 0),
+    (cfg_of("m2", 48, 4, 128, 64, "fp8"), [(500, 40), (64, 64)], [200, 3000, 65], 0),
+    (cfg_of("m3", 16, 8, 256, 16, "bf16"), [(100, 60), (1500, 40)], [300, 1200], 17),
+    (cfg_of("m4", 8, 2, 64, 16, "bf16"), [(40, 30)], [90, 3, 17], 0),
+    # a prefill batch small enough to split its keys into partitions
+    (cfg_of("m5", 8, 1, 128, 16, "bf16"), [(6000, 64)], [6100, 100], 0),
+    # one of the two batches empty
+    (cfg_of("m6", 16, 2, 128, 16, "bf16"), [(200, 50)], [], 0),
+    (cfg_of("m7", 16, 2, 128, 16, "bf16"), [], [300, 5], 0),
+]
+
+
+@pytest.mark.parametrize("case", MIXED, ids=lambda c: c[0].name)
+def test_mixed_launch_equals_the_separate_calls(case):
+    """mixed_attn returns the separate calls' bits for every interleaving of
+    the two kinds of work, and those match the oracle.  (The decode batches
+    here are small enough that the mixed launch's own partition length, the
+    decode's capped at 2048 keys, is the decode's.)"""
+    from paper_2511_02230_amd import ckv
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    cfg, pf, dc, w = case
+    wl = workload.make_workload(cfg, prefill=pf, decode=dc)
+    say(f"case mixed {cfg.name} prefill={pf} decode={dc} W={w}")
+    dw = DeviceWorkload(wl, "cuda", window=w)
+    st = OracleState(wl, device="cuda")
+    if wl.prefill.num_seqs:
+        dw.append_prefill()
+        st.append_prefill()
+    if wl.decode.num_seqs:
+        dw.append_decode()
+        st.append_decode()
+    torch.cuda.synchronize()
+    H, D = cfg.num_q_heads, cfg.head_dim
+    qp = dw.q_prefill if wl.prefill.num_seqs else torch.empty((0, H, D), dtype=torch.bfloat16, device="cuda")
+    qd = dw.q_decode if wl.decode.num_seqs else torch.empty((0, H, D), dtype=torch.bfloat16, device="cuda")
+    empty = ckv.Batch(torch.zeros((0, 1), dtype=torch.int32, device="cuda"),
+                      torch.zeros(0, dtype=torch.int32, device="cuda"),
+                      torch.zeros(1, dtype=torch.int32, device="cuda"), 0, 0, 0)
+    pbatch = dw.prefill if wl.prefill.num_seqs else empty
+    dbatch = dw.decode if wl.decode.num_seqs else empty
+    for split in (0, 128):
+        ref_p = dw.run_prefill().clone() if wl.prefill.num_seqs else None
+        ref_d = dw.run_decode(kv_split_len=split).clone() if wl.decode.num_seqs else None
+        for inter in (0, 1, 2, 5, 32, 1000):
+            op, od = ckv.mixed_attn(dw.pool, pbatch, qp, dbatch, qd, cfg.softmax_scale, w, split, inter)
+            torch.cuda.synchronize()
+            if ref_p is not None:
+                assert torch.equal(op.view(torch.int16), ref_p.view(torch.int16)), (split, inter)
+            if ref_d is not None:
+                assert torch.equal(od.view(torch.int16), ref_d.view(torch.int16)), (split, inter)
+        if ref_p is not None:
+            ref = st.prefill(to_numpy(dw.q_prefill), st.rows_of(wl.prefill), w)
+            got = out_f64(op)
+            cu = wl.prefill.cu_q_lens
+            for b, r in ref.items():
+                check_close(got[cu[b]:cu[b + 1]], r, cfg, f"mixed prefill seq {b}")
+        if ref_d is not None:
+            ref = st.decode(to_numpy(dw.q_decode), st.rows_of(wl.decode), w)
+            got = out_f64(od)
+            for b, r in ref.items():
+                check_close(got[b], r, cfg, f"mixed decode seq {b} split {split}")
+
+
+@pytest.mark.parametrize("name", ["llama3.1-70b", "glm4.5-355b"])
+def test_mixed_launch_full_config(name):
+    """The benchmark's mixed step at full size (decode partitions of 2048
+    keys, the mixed launch's own choice there): bit-identical to the
+    separate calls at that length, and sampled rows within the bars of the
+    oracle."""
+    from paper_2511_02230_amd import ckv
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    cfg = workload.CONFIGS[name]
+    wl = workload.make_workload(cfg)
+    rng = np.random.default_rng([cfg.seed, 0, 11])
+    pf_rows, dc_rows, subsets = _sample_rows(wl, rng)
+    say(f"case mixed full {name}")
+    dw = DeviceWorkload(wl, "cuda")
+    dw.append_prefill()
+    dw.append_decode()
+    ref_p = dw.run_prefill().clone()
+    ref_d = dw.run_decode(kv_split_len=2048).clone()
+    op, od = ckv.mixed_attn(dw.pool, dw.prefill, dw.q_prefill, dw.decode, dw.q_decode, cfg.softmax_scale)
+    torch.cuda.synchronize()
+    assert torch.equal(op.view(torch.int16), ref_p.view(torch.int16))
+    assert torch.equal(od.view(torch.int16), ref_d.view(torch.int16))
+    op2, od2 = ckv.mixed_attn(dw.pool, dw.prefill, dw.q_prefill, dw.decode, dw.q_decode, cfg.softmax_scale,
+                              kv_split_len=2048, interleave=32)
+    torch.cuda.synchronize()
+    assert torch.equal(op2.view(torch.int16), ref_p.view(torch.int16))
+    assert torch.equal(od2.view(torch.int16), ref_d.view(torch.int16))
+    sids = sorted(set(int(wl.prefill.seq_ids[b]) for b in pf_rows) | set(int(wl.decode.seq_ids[b]) for b in dc_rows))
+    st = OracleState(wl, sids=sids, device="cuda")
+    st.append_prefill(pf_rows)
+    st.append_decode(dc_rows)
+    ref = st.prefill(to_numpy(dw.q_prefill), [b for b in pf_rows if b in st.rows_of(wl.prefill)], 0, subsets)
+    got = out_f64(op)
+    cu = wl.prefill.cu_q_lens
+    for b, r in ref.items():
+        check_close(got[cu[b] + subsets[b]], r, cfg, f"mixed prefill seq {b}")
+    ref = st.decode(to_numpy(dw.q_decode), st.rows_of(wl.decode, dc_rows))
+    got = out_f64(od)
+    for b, r in ref.items():
+        check_close(got[b], r, cfg, f"mixed decode seq {b}")
