@@ -219,6 +219,8 @@ def main():
     w = args.window
     # the stored traffic was measured on the default workload only
     default_cfg = args.config == "llama3.1-70b" and w == 0
+    if mixed is not None:
+        mixed["traffic"] = measured_traffic("mixed_attn") if default_cfg else None
     flops = prefill_flops(wl, w)
     dbytes = decode_bytes(wl, w)
     abytes = append_bytes(wl, wl.prefill.total_q)
@@ -236,7 +238,9 @@ def main():
                               "traffic": measured_traffic("paged_decode_attn") if default_cfg else None,
                               "ms": per["paged_decode_attn"], "work": dbytes},
         "kv_append": {"bound": "hbm", "achieved": app_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                      "frac": app_gbs / PEAK_HBM_GBS, "traffic": None, "ms": per["kv_append_prefill"],
+                      "frac": app_gbs / PEAK_HBM_GBS,
+                      "traffic": measured_traffic("kv_append") if default_cfg else None,
+                      "ms": per["kv_append_prefill"],
                       "work": abytes},
         "kv_append_decode": {"bound": "hbm", "ms": per["kv_append_decode"], "work": adbytes},
     }

@@ -101,7 +101,25 @@ __device__ __forceinline__ u32x2 ds_read_tr16(const lds_u8 *p) {
   const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)(p));
   return __builtin_bit_cast(u32x2, v);
 }
+// Transposed 8-bit read: within each 16-lane group, lane i = 2m + h of the
+// group names an 8-byte run; lane 8h + k of the group receives byte k of the
+// runs of lanes h, 2 + h, ..., 14 + h (byte m from lane 2m + h).  With lane
+// 2m + h pointing at row m, columns 8h .. 8h + 7 of a row-major byte matrix,
+// group lane o gets column o of rows 0..7 (layout checked on the GPU).
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) i32x2 lds_i32x2_t;
+__device__ __forceinline__ u32x2 ds_read_tr8(const lds_u8 *p) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2_t *)(p)));
+}
 __device__ __forceinline__ u32x4 lds_ld16(const lds_u8 *p) { return *(const lds_u32x4_t *)(p); }
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2_t;
+__device__ __forceinline__ u32x2 lds_ld8(const lds_u8 *p) { return *(const lds_u32x2_t *)(p); }
+
+// Eight E4M3FN codes (8 bytes of LDS) -> one 16-byte chunk of bf16 values.
+__device__ __forceinline__ u32x4 fp8x8_to_bf16x8(u32x2 codes) {
+  const u32x2 a = fp8x4_to_bf16x4(codes.x), b = fp8x4_to_bf16x4(codes.y);
+  return u32x4{a.x, a.y, b.x, b.y};
+}
 __device__ __forceinline__ void lds_st16(lds_u8 *p, u32x4 v) { *(lds_u32x4_t *)(p) = v; }
 
 // Read-only tables (block table, fp8 scales) are read through the constant

@@ -169,18 +169,15 @@ __device__ __forceinline__ void compute_block(const DecodeArgs &a, const DState<
 
   const lds_u8 *vb = stage;
   if constexpr (FP8) {
-    // widen the block's V codes into bf16 rows (swizzled like a bf16 block)
+    // widen the block's V codes into bf16 rows (swizzled like a bf16 block):
+    // each lane turns 8 codes into one 16-byte chunk, so every 8 and 16
+    // consecutive lanes store to distinct 16-byte bank groups
 #pragma unroll
-    for (int it = 0; it < C::VRAW / 1024; ++it) {
+    for (int it = 0; it < C::KB * C::ROW / 1024; ++it) {
       const int id = lane + 64 * it;
-      const int row = id / C::RCH, cc = id % C::RCH;
-      const u32x4 x = lds_ld16(stage + row * C::RAW_ROW + cc * 16);
-      const u32x2 a0 = fp8x4_to_bf16x4(x.x), a1 = fp8x4_to_bf16x4(x.y);
-      const u32x2 b0 = fp8x4_to_bf16x4(x.z), b1 = fp8x4_to_bf16x4(x.w);
-      lds_u8 *dst = vwide + row * C::ROW;
-      const int sw = vswz<C::CH>(row);
-      lds_st16(dst + (((2 * cc) ^ sw) << 4), u32x4{a0.x, a0.y, a1.x, a1.y});
-      lds_st16(dst + (((2 * cc + 1) ^ sw) << 4), u32x4{b0.x, b0.y, b1.x, b1.y});
+      const int row = id / C::CH, cc = id % C::CH;
+      const u32x4 w = fp8x8_to_bf16x8(lds_ld8(stage + row * C::RAW_ROW + cc * 8));
+      lds_st16(vwide + row * C::ROW + ((cc ^ vswz<C::CH>(row)) << 4), w);
     }
     vb = vwide;
   }

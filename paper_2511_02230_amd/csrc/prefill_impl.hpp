@@ -17,8 +17,12 @@
 //     is computed, in one burst after the barrier (head_dim 256: in three
 //     parts spread over the step, as one wave per SIMD has no partner wave
 //     to cover the burst).
-//   * fp8 pools are loaded raw, then widened to bf16 (exactly) once per
-//     workgroup into a bf16 block with the same layout.
+//   * fp8 pools stay raw in LDS.  Each wave widens the codes of its own
+//     operands in registers (exactly: every E4M3 value is a bf16 value): K
+//     16 codes per read (two k-steps; Q is loaded in the matching order of
+//     d), V^T 8 codes per ds_read_b64_tr_b8 (8 keys of one column).  There
+//     is no widening pass and no second barrier, and the operand reads move
+//     half the LDS bytes of the bf16 path.
 // Math, per wave of 32 rows:
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (Q stays in registers).  The
 //     lane that owns a query row holds a column of S^T, so the row max / row
@@ -80,6 +84,7 @@ struct Cfg {
   static constexpr int ROW = D * 2;                    // bf16 bytes per key row in LDS
   static constexpr int CH = D / 8;                     // 16-byte chunks per bf16 row
   static constexpr int BN_ = BN;                       // keys per block
+  static constexpr bool F8 = FP8;                      // raw fp8 rows in LDS
   static constexpr int BLK = BN * ROW;                 // bf16 bytes of one K (or V) block
   static constexpr int RAW_ROW = FP8 ? D : D * 2;      // pool bytes per key row
   static constexpr int RCH = RAW_ROW / 16;             // 16-byte chunks per pool row
@@ -95,8 +100,8 @@ struct Cfg {
   // so a third goes out after the barrier, a third after the first S^T half
   // and the rest inside PV; with two waves per SIMD one burst is faster.
   static constexpr int SPREAD = (D >= 256 && !FP8) ? 3 : 1;
-  // two-stage K ring + two-stage V ring (+ the widened bf16 K and V blocks for fp8)
-  static constexpr int LDS = 4 * RAW_BLK + (FP8 ? 2 * BLK : 0);
+  // two-stage K ring + two-stage V ring
+  static constexpr int LDS = 4 * RAW_BLK;
   static_assert(RAW_BLK % 2048 == 0, "each wave issues whole 1-KB loads");
   static_assert(PS % RPD == 0, "a load never straddles a page");
   // two workgroups per CU below head_dim 256; one (as the registers allow) above
@@ -112,6 +117,18 @@ template <int CH>
 __device__ __forceinline__ int swz_k(int key) { return key & ((CH < 16 ? CH : 16) - 1); }
 template <int CH>
 __device__ __forceinline__ int swz_v(int key) { return (4 * (key & 3)) & (CH - 1); }
+
+// XOR swizzles of the 16-byte chunk index within a raw fp8 row (RCH chunks).
+//  K: a lane reads 16 codes (two k-steps) of key pi(col); the 8 keys of each
+//     8-lane group (pi of 0-7 or 8-15 within 16) and the even and the odd
+//     keys among 16 lanes land on distinct chunks.
+//  V: a transposed 8-bit read covers 8 consecutive keys x two 8-byte runs
+//     per 16 lanes; shifting key k's chunks by k & 7 spreads them over all
+//     sixteen 8-byte bank groups of a 128-byte row.
+template <int RCH>
+__device__ __forceinline__ int swz8_k(int key) { return (((key >> 1) ^ ((key & 1) << 1)) & 7) & (RCH - 1); }
+template <int RCH>
+__device__ __forceinline__ int swz8_v(int key) { return key & 7 & (RCH - 1); }
 
 // Workgroup barrier without a memory fence: LDS reads of this wave are
 // complete (lgkmcnt 0) and the compiler may not move memory accesses across.
@@ -140,8 +157,8 @@ __device__ __forceinline__ void lane_offsets(uint32_t (&loff)[C::DPW]) {
   for (int i = 0; i < C::DPW; ++i) {
     const int row = h * HROWS + i * C::RPD + lane / C::RCH;  // row within the block
     const int slot = lane % C::RCH;
-    int chunk = slot;
-    if constexpr (!FP8) chunk = slot ^ (t == 0 ? swz_k<C::CH>(row) : swz_v<C::CH>(row));
+    const int chunk = FP8 ? slot ^ (t == 0 ? swz8_k<C::RCH>(row) : swz8_v<C::RCH>(row))
+                          : slot ^ (t == 0 ? swz_k<C::CH>(row) : swz_v<C::CH>(row));
     loff[i] = (uint32_t)(((i % DPP) * C::RPD + lane / C::RCH) * C::RAW_ROW + chunk * 16);
   }
 }
@@ -205,24 +222,6 @@ __device__ __forceinline__ void issue_block(const PrefillArgs &a, const int32_t 
 }
 
 
-// fp8: widen one raw block of a tensor into its bf16 block (same layout as a
-// bf16 block, swizzle included); all four waves share the work.
-template <class C>
-__device__ __forceinline__ void widen(const lds_u8 *raw, lds_u8 *dst16, bool is_k) {
-#pragma unroll
-  for (int it = 0; it < C::RAW_BLK / (16 * kThreads); ++it) {
-    const int id = threadIdx.x + kThreads * it;
-    const int row = id / C::RCH, c = id % C::RCH;
-    const u32x4 x = lds_ld16(raw + row * C::RAW_ROW + c * 16);
-    const u32x2 a0 = fp8x4_to_bf16x4(x.x), a1 = fp8x4_to_bf16x4(x.y);
-    const u32x2 b0 = fp8x4_to_bf16x4(x.z), b1 = fp8x4_to_bf16x4(x.w);
-    lds_u8 *dst = dst16 + row * C::ROW;
-    const int sw = is_k ? swz_k<C::CH>(row) : swz_v<C::CH>(row);
-    lds_st16(dst + (((2 * c) ^ sw) << 4), u32x4{a0.x, a0.y, a1.x, a1.y});
-    lds_st16(dst + (((2 * c + 1) ^ sw) << 4), u32x4{b0.x, b0.y, b1.x, b1.y});
-  }
-}
-
 // Exchange between lane l and lane l ^ 32 (the two halves of a wave).
 __device__ __forceinline__ float half_swap_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -254,6 +253,20 @@ struct Tile {
 
 template <class C>
 __device__ __forceinline__ void lds_offsets(Tile<C> &T) {
+  if constexpr (C::F8) {
+    // K: the 16 codes of k-steps 2p, 2p+1 of key pi(col) (chunk 2p + half);
+    // V^T: group lane 2m + h names key 8 (gq / 2) + m, columns
+    // 32 dt + 16 (gq & 1) + 8 h .. + 7 (chunk 2 dt + (gq & 1), run h)
+    const int key = pi_row(T.col);
+#pragma unroll
+    for (int p = 0; p < C::DS / 2; ++p)
+      T.offk[p] = key * C::RAW_ROW + (((2 * p + T.half) ^ swz8_k<C::RCH>(key)) << 4);
+    const int vkey = 8 * (T.gq >> 1) + (T.li >> 1);
+#pragma unroll
+    for (int dt = 0; dt < C::DT; ++dt)
+      T.offv[dt] = vkey * C::RAW_ROW + (((2 * dt + (T.gq & 1)) ^ swz8_v<C::RCH>(vkey)) << 4) + 8 * (T.li & 1);
+    return;
+  }
   const int key0 = 8 * (T.gq >> 1) + (T.li >> 2);
   const int dsub = 16 * (T.gq & 1) + 4 * (T.li & 3);
 #pragma unroll
@@ -273,6 +286,25 @@ __device__ __forceinline__ void lds_offsets(Tile<C> &T) {
 // accumulation chains.  Row m of tile tt is key 32 tt + pi(m).
 template <class C, int P>
 __device__ __forceinline__ void qk_part(const lds_u8 *kb, const Tile<C> &T, f32x16 (&s)[C::NT]) {
+  if constexpr (C::F8) {
+    // one 16-code read per tile feeds k-steps 2p and 2p + 1
+#pragma unroll
+    for (int pp = 0; pp < C::DS / 4; ++pp) {
+      const int p = P * (C::DS / 4) + pp;
+      u32x4 x[C::NT];
+#pragma unroll
+      for (int tt = 0; tt < C::NT; ++tt) x[tt] = lds_ld16(kb + T.offk[p] + 32 * tt * C::RAW_ROW);
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int tt = 0; tt < C::NT; ++tt) {
+          if (p == 0 && e == 0) s[tt] = f32x16{};
+          const u32x4 w = fp8x8_to_bf16x8(e ? u32x2{x[tt].z, x[tt].w} : u32x2{x[tt].x, x[tt].y});
+          s[tt] = mfma32x32x16(as_bf16x8(w), T.qf[2 * p + e], s[tt]);
+        }
+    }
+    return;
+  }
 #pragma unroll
   for (int n = 0; n < C::NQK / 2; ++n) {
     const int tt = n % C::NT, ds = P * (C::DS / 2) + n / C::NT;
@@ -351,10 +383,16 @@ template <class C>
 __device__ __forceinline__ void pv_slice(Tile<C> &T, const lds_u8 *vb, int tt, int ks, const u32x4 &pb) {
 #pragma unroll
   for (int dt = 0; dt < C::DT; ++dt) {
-    const lds_u8 *r0 = vb + T.offv[dt] + (32 * tt + 16 * ks) * C::ROW;
-    const u32x2 lo = ds_read_tr16(r0);
-    const u32x2 hi = ds_read_tr16(r0 + 4 * C::ROW);
-    const u32x4 vx = {lo.x, lo.y, hi.x, hi.y};
+    u32x4 vx;
+    if constexpr (C::F8) {
+      // 8 keys of one column, widened in registers
+      vx = fp8x8_to_bf16x8(ds_read_tr8(vb + T.offv[dt] + (32 * tt + 16 * ks) * C::RAW_ROW));
+    } else {
+      const lds_u8 *r0 = vb + T.offv[dt] + (32 * tt + 16 * ks) * C::ROW;
+      const u32x2 lo = ds_read_tr16(r0);
+      const u32x2 hi = ds_read_tr16(r0 + 4 * C::ROW);
+      vx = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
     T.o[dt] = mfma32x32x16(as_bf16x8(vx), as_bf16x8(pb), T.o[dt]);
   }
 }
@@ -512,7 +550,7 @@ __device__ __forceinline__ void softmax_pv(const PrefillArgs &a, const int32_t *
 // of blocks j and j+1.  Stage of block b: b & 1 in both rings.
 template <class C>
 struct Rings {
-  lds_u8 *k, *v, *k16, *v16;
+  lds_u8 *k, *v;
   __device__ __forceinline__ lds_u8 *kst(int b) const { return k + (b & 1) * C::RAW_BLK; }
   __device__ __forceinline__ lds_u8 *vst(int b) const { return v + (b & 1) * C::RAW_BLK; }
 };
@@ -553,13 +591,6 @@ __device__ __forceinline__ void step(const PrefillArgs &a, const int32_t *bt, Ti
   wait_and_issue<C, PS, FP8, U>(a, bt, T, j, R);
   const lds_u8 *kb = R.k + (U ^ 1) * C::RAW_BLK;  // K of block j+1
   const lds_u8 *vb = R.v + U * C::RAW_BLK;        // V of block j
-  if constexpr (FP8) {
-    widen<C>(kb, R.k16, true);
-    widen<C>(vb, R.v16, false);
-    lds_barrier();
-    kb = R.k16;
-    vb = R.v16;
-  }
   float ksc[C::NT * 2], vsc[C::NT * 2];
   scale_mask<C, PS, FP8>(a, bt, T, j, s_cur, ksc, vsc);
   // (past the last block this reads a stale K stage; the result is unused)
@@ -576,8 +607,6 @@ __device__ __forceinline__ void prefill_tile(const PrefillArgs &a, lds_u8 *lds, 
   Rings<C> R;
   R.k = lds;
   R.v = R.k + 2 * C::RAW_BLK;
-  R.k16 = R.v + 2 * C::RAW_BLK;  // fp8 only
-  R.v16 = R.k16 + C::BLK;
 
   // hx = H_kv * split + g (KV head fastest); with splits > 1 each item
   // covers one key partition
@@ -664,10 +693,13 @@ __device__ __forceinline__ void prefill_tile(const PrefillArgs &a, lds_u8 *lds, 
     block_pages<C, PS>(bt, T.kb_begin * BN, T.kv_end, T.pg);
     issue_block<C, PS, FP8>(a, bt, g, T.kb_begin * BN, T.kv_end, T.pg, T.loff, R.k);
   }
+  // k-step s takes d = 16 s + 8 half + 0..7; fp8 pools pair the steps so
+  // that one 16-code K read feeds two: d = 32 (s / 2) + 16 half + 8 (s % 2)
 #pragma unroll
   for (int s = 0; s < C::DS; ++s) {
+    const int d0 = FP8 ? 32 * (s >> 1) + 16 * T.half + 8 * (s & 1) : 16 * s + 8 * T.half;
     u32x4 x = {0u, 0u, 0u, 0u};
-    if (rvalid) x = ld<u32x4>(a.q + qrow + 16 * s + 8 * T.half);
+    if (rvalid) x = ld<u32x4>(a.q + qrow + d0);
     T.qf[s] = as_bf16x8(x);
   }
 #pragma unroll
@@ -677,16 +709,8 @@ __device__ __forceinline__ void prefill_tile(const PrefillArgs &a, lds_u8 *lds, 
 
   f32x16 sA[C::NT], sB[C::NT];
   wait_and_issue<C, PS, FP8, 1, true>(a, bt, T, -1, R);  // U = (-1) & 1
-  {
-    const lds_u8 *kb = R.k;
-    if constexpr (FP8) {
-      widen<C>(R.k, R.k16, true);
-      lds_barrier();
-      kb = R.k16;
-    }
-    qk_part<C, 0>(kb, T, sA);
-    qk_part<C, 1>(kb, T, sA);
-  }
+  qk_part<C, 0>(R.k, T, sA);
+  qk_part<C, 1>(R.k, T, sA);
 
   for (int j0 = 0; j0 < T.nblk; j0 += 2) {
     step<C, PS, FP8, 0>(a, bt, T, j0, sA, sB, R);
