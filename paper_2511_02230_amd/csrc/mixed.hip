@@ -22,7 +22,8 @@
 // prefill tiles and let decode workgroups take the slots that finishing
 // tiles free.  Measured at the Llama-3.1-70B step (one process, 20 reps):
 // 9.2-9.5 ms for runs of 96-192 groups against 9.9-10.1 ms for the two
-// kernels back to back; runs of 32 gave 9.4-9.8.
+// kernels back to back; runs of 32 gave 9.4-9.8.  A batch whose decode is a
+// small part of the work runs all prefill groups first (see launch_mixed).
 #include <algorithm>
 
 #include "args.hpp"
@@ -44,7 +45,7 @@ struct MixedLayout {
 // pf_groups + dc_groups, so every group of either kind gets one position.
 __device__ __forceinline__ int dc_before(const MixedLayout &m, int i) {
   const int h = m.half;
-  long long pat = (long long)h * (i / (2 * h)) + max(0, i % (2 * h) - h);
+  long long pat = (long long)h * (i / (2LL * h)) + max(0LL, i % (2LL * h) - h);
   pat = max(pat, (long long)i - m.pf_groups);
   return (int)min(pat, (long long)m.dc_groups);
 }
@@ -135,9 +136,21 @@ hipError_t launch_mixed(const PoolView &p, const BatchView &pb, const void *q_pf
   const long long total = (long long)m.pf_groups + m.dc_groups;
   if (total == 0) return hipSuccess;
   if (8 * total > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  // default runs: three fills of the GPU (256 CUs, two workgroups per CU
-  // below head_dim 256) in groups of eight workgroups
-  m.half = interleave > 0 ? interleave : 3 * (p.d >= 256 ? 1 : 2) * 256 / 8;
+  // Default runs: three fills of the GPU (256 CUs, two workgroups per CU
+  // below head_dim 256) in groups of eight workgroups.  When the decode is a
+  // small part of the step (its bytes at ~6.5 TB/s under 5 % of the prefill's
+  // flops at ~1.1 PFLOP/s, both from the host-side bounds), all prefill
+  // groups go first and the decode only fills the prefill's tail: at
+  // GLM-4.5 (2 ms of decode in a 270 ms step) interleaving cost more than it
+  // saved (272.1 ms prefill-first, 273.1 in runs of 192, 272.9 back to back).
+  if (interleave > 0) {
+    m.half = interleave;
+  } else {
+    const double e_kv = p.kv_dtype == 2 ? 1.0 : 2.0;
+    const double pf_s = has_pf ? 4.0 * p.d * h_q * pb.total_q * ((double)pb.max_ctx + pb.max_q) / 1.1e15 : 0.0;
+    const double dc_s = has_dc ? (double)db.num_seqs * db.max_ctx * p.h_kv * p.d * 2.0 * e_kv / 6.5e12 : 0.0;
+    m.half = dc_s < 0.05 * pf_s ? 0x3fffffff : 3 * (p.d >= 256 ? 1 : 2) * 256 / 8;
+  }
   const bool fp8 = p.kv_dtype == 2;
   hipError_t e = hipErrorInvalidValue;
   switch (p.d) {
