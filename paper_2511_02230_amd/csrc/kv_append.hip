@@ -16,6 +16,9 @@ struct AppendArgs {
   int32_t units;       // 16-byte input chunks per (token, head) row
   int32_t in_row, out_row;  // bytes per (token, head) row in the input / pool
   int32_t tok_per_block;
+  // log2 of units, h and ps when all three are powers of two (else -1): the
+  // chunk index then splits by shifts and masks instead of divisions
+  int32_t lg_units, lg_h, lg_ps;
 };
 
 // Quantize 8 bf16 values (one 16-byte chunk) to 8 E4M3FN codes:
@@ -60,6 +63,29 @@ __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
   const int per_tok = 2 * per_kv;
   const int total = tcount * per_tok;
   const int32_t *bt = a.bt + (size_t)b * a.max_pages;
+  if (a.lg_units >= 0) {
+    // power-of-two shapes: u = ((tt * 2 + kv) * h + hh) * units + c
+    const int lu = a.lg_units, lh = a.lg_h, lp = a.lg_ps;
+    for (int u = threadIdx.x; u < total; u += blockDim.x) {
+      const int c = u & (per_head - 1);
+      const int hh = (u >> lu) & (a.h - 1);
+      const int kv = (u >> (lu + lh)) & 1;
+      const int t = t0 + (u >> (lu + lh + 1));
+      const int pos = P + t;
+      const int page = bt[pos >> lp];
+      const int slot = pos & (a.ps - 1);
+      const uint8_t *src = (kv ? a.v_new : a.k_new) + ((size_t)(q0 + t) * a.h + hh) * a.in_row + c * 16;
+      uint8_t *dst = (kv ? a.v_pool : a.k_pool) + (((size_t)page * a.h + hh) * a.ps + slot) * a.out_row;
+      const u32x4 x = ld<u32x4>(src);
+      if constexpr (!FP8) {
+        st<u32x4>(dst + c * 16, x);
+      } else {
+        const float s = (kv ? a.v_scale : a.k_scale)[(size_t)page * a.h + hh];
+        st<u32x2>(dst + c * 8, quantize8(x, s));
+      }
+    }
+    return;
+  }
   for (int u = threadIdx.x; u < total; u += blockDim.x) {
     const int tt = u / per_tok;
     int r = u - tt * per_tok;
@@ -109,6 +135,15 @@ hipError_t launch_kv_append(const PoolView &p, const BatchView &b, const void *k
   a.units = a.in_row / 16;
   const int per_tok = 2 * p.h_kv * a.units;
   a.tok_per_block = per_tok >= 1024 ? 1 : 1024 / per_tok;
+  auto lg = [](int x) {
+    int l = 0;
+    while ((1 << l) < x) ++l;
+    return (1 << l) == x ? l : -1;
+  };
+  a.lg_units = lg(a.units);
+  a.lg_h = lg(a.h);
+  a.lg_ps = lg(a.ps);
+  if (a.lg_h < 0 || a.lg_ps < 0) a.lg_units = -1;
   dim3 grid((b.max_q + a.tok_per_block - 1) / a.tok_per_block, b.num_seqs);
   if (fp8)
     hipLaunchKernelGGL(kv_append_kernel<true>, grid, dim3(256), 0, s, a);

@@ -157,6 +157,9 @@ SMALL = [
     # decode covers the group in two head chunks, the second one ragged
     (cfg_of("g1", 40, 2, 128, 16, "bf16"), [(90, 33), (0, 7)], [1, 77, 300], 0),
     (cfg_of("g2", 40, 2, 128, 64, "fp8"), [(150, 21)], [64, 129], 0),
+    # three KV heads: the append's index math without power-of-two shifts
+    (cfg_of("h3", 6, 3, 128, 16, "bf16"), [(40, 20), (3, 30)], [50, 17], 0),
+    (cfg_of("h3f8", 12, 3, 128, 64, "fp8"), [(70, 9)], [80], 0),
     (cfg_of("f1", 4, 2, 64, 16, "f32", "f32"), [(30, 20), (0, 3)], [19, 50], 0),
     (cfg_of("f2", 4, 1, 128, 64, "f32", "f32"), [(70, 9)], [129], 5),
 ]
