@@ -202,19 +202,32 @@ def main():
             ckv.mixed_attn(dw.pool, dw.prefill, dw.q_prefill, dw.decode, dw.q_decode, cfg.softmax_scale,
                            args.window, out_prefill=op, out_decode=od, workspace=mws)
 
-        for _ in range(args.warmup):
-            mixed_step()
-        torch.cuda.synchronize()
-        m0 = torch.cuda.Event(enable_timing=True)
-        m1 = torch.cuda.Event(enable_timing=True)
-        m0.record(stream)
-        for _ in range(args.steps):
-            mixed_step()
-        m1.record(stream)
-        torch.cuda.synchronize()
-        mixed_ms = m0.elapsed_time(m1) / args.steps
+        def time_steps(fn):
+            for _ in range(args.warmup):
+                fn()
+            torch.cuda.synchronize()
+            m0 = torch.cuda.Event(enable_timing=True)
+            m1 = torch.cuda.Event(enable_timing=True)
+            m0.record(stream)
+            for _ in range(args.steps):
+                fn()
+            m1.record(stream)
+            torch.cuda.synchronize()
+            return m0.elapsed_time(m1) / args.steps
+
+        mixed_ms = time_steps(mixed_step)
         mixed = {"ms_per_step": mixed_ms, "sequential_ms_per_step": ms_step, "speedup": ms_step / mixed_ms,
                  "launch": "kv_append x2 + mixed_attn (prefill row tiles and decode partitions in one grid)"}
+        if cfg.kv_dtype == "bf16":
+            # the whole step in one launch: mixed_attn given the new rows
+            # writes them into the pool itself (the same pool contents)
+            def fused_step():
+                ckv.mixed_attn(dw.pool, dw.prefill, dw.q_prefill, dw.decode, dw.q_decode, cfg.softmax_scale,
+                               args.window, out_prefill=op, out_decode=od, workspace=mws,
+                               k_prefill=dw.k_new, v_prefill=dw.v_new, k_decode=dw.k_dec, v_decode=dw.v_dec)
+
+            mixed["fused_append_ms_per_step"] = time_steps(fused_step)
+            mixed["fused_append_launch"] = "mixed_attn given the new K/V rows (the appends inside the same launch)"
 
     w = args.window
     # the stored traffic was measured on the default workload only

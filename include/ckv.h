@@ -197,8 +197,21 @@ ckv_status_t paged_decode_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
  * Results are those of the two separate calls, bit for bit (same work
  * items, same key partitions), with the same argument rules; `prefill`
  * follows prefix_prefill_attn's batch conventions and `decode`
- * paged_decode_attn's.  Both read the pool only: append both batches' new
- * K/V first.  Either batch may be empty (num_seqs 0).
+ * paged_decode_attn's.  Either batch may be empty (num_seqs 0).
+ *   k_prefill / v_prefill, k_decode / v_decode: the new K and V rows, or
+ *   both NULL when kv_append has already put them in the pool.  Given, the
+ *   launch appends them itself (the append fused into the attention: each
+ *   row is written into its pool slot by one work item, and the work items
+ *   that need it read it from these rows), leaving the pool and the outputs
+ *   exactly as kv_append followed by this call.  Prefill rows are
+ *   [total_q_len][H_kv][D] as for kv_append (ctx_lens = P_b, the tokens
+ *   before the turn); decode rows are [num_seqs][H_kv][D], the token at
+ *   position ctx_lens[b] - 1 (ctx_lens counts it, as in paged_decode_attn).
+ *   bf16 pools only (bf16 rows): an fp8 pool returns CKV_ERR_UNSUPPORTED,
+ *   since every work item reading a new key would have to encode it again.
+ *   One of a pair NULL returns CKV_ERR_INVALID_ARG.  The rows must not
+ *   alias the pool, and the two batches must not share the pool slots the
+ *   appended rows go to.
  *   q_dtype: CKV_BF16 (bf16 or fp8 pools); other types return
  *   CKV_ERR_UNSUPPORTED.
  *   kv_split_len: the decode's partition length, as for paged_decode_attn;
@@ -213,11 +226,12 @@ ckv_status_t paged_decode_attn(const ckv_pool_t *pool, const ckv_batch_t *batch,
  *   aligned (the prefill's partials, then the decode's).
  */
 ckv_status_t mixed_attn(const ckv_pool_t *pool, const ckv_batch_t *prefill, const void *q_prefill,
-                        void *out_prefill, const ckv_batch_t *decode, const void *q_decode,
-                        void *out_decode, ckv_dtype_t q_dtype, int32_t num_q_heads,
-                        float softmax_scale, int32_t window, int32_t kv_split_len,
-                        int32_t interleave, void *workspace, size_t workspace_bytes,
-                        hipStream_t stream);
+                        const void *k_prefill, const void *v_prefill, void *out_prefill,
+                        const ckv_batch_t *decode, const void *q_decode, const void *k_decode,
+                        const void *v_decode, void *out_decode, ckv_dtype_t q_dtype,
+                        int32_t num_q_heads, float softmax_scale, int32_t window,
+                        int32_t kv_split_len, int32_t interleave, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream);
 size_t mixed_attn_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t *prefill,
                                   const ckv_batch_t *decode, int32_t num_q_heads,
                                   int32_t kv_split_len);

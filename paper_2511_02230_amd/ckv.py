@@ -60,7 +60,8 @@ def _load():
         "prefix_prefill_attn": ([P, B, vp, ctypes.c_int, i32, f32, i32, vp, vp, sz, vp], ctypes.c_int),
         "paged_decode_attn": ([P, B, vp, ctypes.c_int, i32, f32, i32, i32, vp, vp, sz, vp], ctypes.c_int),
         "paged_decode_attn_noalloc": ([P, B, vp, ctypes.c_int, i32, f32, i32, i32, vp, vp], ctypes.c_int),
-        "mixed_attn": ([P, B, vp, vp, B, vp, vp, ctypes.c_int, i32, f32, i32, i32, i32, vp, sz, vp],
+        "mixed_attn": ([P, B, vp, vp, vp, vp, B, vp, vp, vp, vp, ctypes.c_int, i32, f32, i32, i32, i32, vp, sz,
+                        vp],
                        ctypes.c_int),
         "mixed_attn_workspace_bytes": ([P, B, B, i32, i32], sz),
         "prefix_prefill_workspace_bytes": ([P, B, i32], sz),
@@ -253,18 +254,36 @@ def mixed_workspace_bytes(pool: Pool, prefill: Batch, decode: Batch, num_q_heads
                                               num_q_heads, kv_split_len))
 
 
+def _append_rows(pool: Pool, k, v, n: int, name: str):
+    """The fused append's new rows: both None, or bf16 [n, H_kv, D] each."""
+    if (k is None) != (v is None):
+        raise ValueError(f"{name}: give both K and V rows, or neither")
+    if k is None:
+        return None, None
+    for t, nm in ((k, "k"), (v, "v")):
+        _dev(t, f"{nm}_{name}", torch.bfloat16)
+        if tuple(t.shape) != (n, pool.k.shape[1], pool.k.shape[3]):
+            raise ValueError(f"{nm}_{name} must be [{n}, H_kv, D]")
+    return k, v
+
+
 def mixed_attn(pool: Pool, prefill: Batch, q_prefill: torch.Tensor, decode: Batch, q_decode: torch.Tensor,
                softmax_scale: float, window: int = 0, kv_split_len: int = 0, interleave: int = 0,
-               out_prefill=None, out_decode=None, workspace=None, stream=None):
+               out_prefill=None, out_decode=None, workspace=None, stream=None,
+               k_prefill=None, v_prefill=None, k_decode=None, v_decode=None):
     """Prefill over `prefill` (q_prefill [total_q_len, H_q, D]) and decode over
     `decode` (q_decode [num_seqs, H_q, D]) in one launch; returns
-    (out_prefill, out_decode)."""
+    (out_prefill, out_decode).  k_/v_prefill ([total_q_len, H_kv, D]) and
+    k_/v_decode ([num_seqs, H_kv, D]), bf16 pools only: new rows that the
+    launch appends to the pool itself (else the pool already holds them)."""
     _dev(q_prefill, "q_prefill", torch.bfloat16)
     _dev(q_decode, "q_decode", torch.bfloat16)
     if q_prefill.dim() != 3 or q_prefill.shape[0] != prefill.total_q_len:
         raise ValueError("q_prefill must be [total_q_len, H_q, D]")
     if q_decode.dim() != 3 or q_decode.shape[0] != decode.num_seqs or q_decode.shape[1:] != q_prefill.shape[1:]:
         raise ValueError("q_decode must be [num_seqs, H_q, D]")
+    k_prefill, v_prefill = _append_rows(pool, k_prefill, v_prefill, prefill.total_q_len, "prefill")
+    k_decode, v_decode = _append_rows(pool, k_decode, v_decode, decode.num_seqs, "decode")
     out_prefill = _out_like(q_prefill, out_prefill)
     out_decode = _out_like(q_decode, out_decode)
     h_q = q_prefill.shape[1]
@@ -272,9 +291,10 @@ def mixed_attn(pool: Pool, prefill: Batch, q_prefill: torch.Tensor, decode: Batc
                          q_prefill.device)
     pc, pb, db = pool.c(), prefill.c(), decode.c()
     _check("mixed_attn", LIB.mixed_attn(
-        ctypes.byref(pc), ctypes.byref(pb), _ptr(q_prefill), _ptr(out_prefill), ctypes.byref(db),
-        _ptr(q_decode), _ptr(out_decode), CKV_BF16, h_q, float(softmax_scale), int(window),
-        int(kv_split_len), int(interleave), _ptr(ws), wsb, _stream(stream)))
+        ctypes.byref(pc), ctypes.byref(pb), _ptr(q_prefill), _ptr(k_prefill), _ptr(v_prefill),
+        _ptr(out_prefill), ctypes.byref(db), _ptr(q_decode), _ptr(k_decode), _ptr(v_decode),
+        _ptr(out_decode), CKV_BF16, h_q, float(softmax_scale), int(window), int(kv_split_len),
+        int(interleave), _ptr(ws), wsb, _stream(stream)))
     return out_prefill, out_decode
 
 

@@ -229,11 +229,12 @@ size_t mixed_attn_workspace_bytes(const ckv_pool_t *pool, const ckv_batch_t *pre
 }
 
 ckv_status_t mixed_attn(const ckv_pool_t *pool, const ckv_batch_t *prefill, const void *q_prefill,
-                        void *out_prefill, const ckv_batch_t *decode, const void *q_decode,
-                        void *out_decode, ckv_dtype_t q_dtype, int32_t num_q_heads,
-                        float softmax_scale, int32_t window, int32_t kv_split_len,
-                        int32_t interleave, void *workspace, size_t workspace_bytes,
-                        hipStream_t stream) {
+                        const void *k_prefill, const void *v_prefill, void *out_prefill,
+                        const ckv_batch_t *decode, const void *q_decode, const void *k_decode,
+                        const void *v_decode, void *out_decode, ckv_dtype_t q_dtype,
+                        int32_t num_q_heads, float softmax_scale, int32_t window,
+                        int32_t kv_split_len, int32_t interleave, void *workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
   CKV_TRY(check_pool(pool));
   CKV_TRY(check_batch(pool, prefill, 0));
   CKV_TRY(check_batch(pool, decode, 1));
@@ -248,15 +249,20 @@ ckv_status_t mixed_attn(const ckv_pool_t *pool, const ckv_batch_t *prefill, cons
   const bool has_dc = decode->num_seqs > 0;
   if (has_pf && (!q_prefill || !out_prefill)) return CKV_ERR_INVALID_ARG;
   if (has_dc && (!q_decode || !out_decode)) return CKV_ERR_INVALID_ARG;
+  // fused append: both rows of a batch or neither, bf16 pools only
+  if (!k_prefill != !v_prefill || !k_decode != !v_decode) return CKV_ERR_INVALID_ARG;
+  if (((has_pf && k_prefill) || (has_dc && k_decode)) && pool->kv_dtype != CKV_BF16)
+    return CKV_ERR_UNSUPPORTED;
   if (has_pf) CKV_TRY(check_prefill_grid(pool, prefill, num_q_heads));
   if (!has_pf && !has_dc) return CKV_OK;
   const size_t need = ckv::mixed_workspace_bytes(view(pool), view(prefill), view(decode),
                                                  num_q_heads, kv_split_len);
   if (need > 0 && (!workspace || workspace_bytes < need)) return CKV_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return CKV_ERR_INVALID_ARG;
-  return launched(ckv::launch_mixed(view(pool), view(prefill), q_prefill, out_prefill, view(decode),
-                                    q_decode, out_decode, num_q_heads, softmax_scale, window,
-                                    kv_split_len, interleave, workspace, stream));
+  return launched(ckv::launch_mixed(view(pool), view(prefill), q_prefill, k_prefill, v_prefill,
+                                    out_prefill, view(decode), q_decode, k_decode, v_decode,
+                                    out_decode, num_q_heads, softmax_scale, window, kv_split_len,
+                                    interleave, workspace, stream));
 }
 
 ckv_status_t paged_decode_attn_noalloc(const ckv_pool_t *pool, const ckv_batch_t *batch,

@@ -127,6 +127,7 @@ void decode_args(const PoolView &p, const BatchView &b, const void *q, int h_q, 
   a.bt = b.bt;
   a.ctx = b.ctx;
   a.max_pages = b.max_pages;
+  a.k_new = a.v_new = nullptr;  // no fused append
   a.h_q = h_q;
   a.h_kv = p.h_kv;
   a.group = h_q / p.h_kv;

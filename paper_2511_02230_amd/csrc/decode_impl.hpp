@@ -49,6 +49,10 @@ struct DecodeArgs {
   int32_t split_len, max_splits, head_chunks;
   float *part_o;   // [B][H_q][max_splits][D]
   float *part_ml;  // [B][H_q][max_splits][2]
+  // fused append (bf16 pools, DCfg::AP): each sequence's new token's K and V
+  // rows [B][H_kv][D], the last context position c - 1; the kernel writes
+  // them into their pool slots and reads that key from here
+  const uint8_t *k_new, *v_new;
 };
 
 constexpr float kRescaleSlack = 8.0f;  // log2 units: defer rescaling below 2^8
@@ -62,8 +66,9 @@ __device__ __forceinline__ int lane_id() {
   return threadIdx.x & 63;
 }
 
-template <int D, bool FP8, int PS>
+template <int D, bool FP8, int PS, bool APPEND = false>
 struct DCfg {
+  static constexpr bool AP = APPEND;              // fused append (bf16 pools)
   static constexpr int KB = D >= 256 ? 16 : 32;   // keys per block
   static constexpr int NT = KB / 16;              // 16-key tiles per block
   static constexpr int RAW_ROW = FP8 ? D : 2 * D; // pool bytes per key row
@@ -81,6 +86,7 @@ struct DCfg {
   static constexpr int LDS = 2 * VRAW + (FP8 ? KB * ROW : 0);
   static_assert(PS % 16 == 0, "tiles never straddle a page");
   static_assert(RPD >= 1 && VLD >= 1, "whole 1-KB loads per tile");
+  static_assert(!(AP && FP8), "the fused append writes bf16 rows");
 };
 
 // d offset of the 8 k-slots a lane (quarter g) supplies at QK^T step `step`.
@@ -114,6 +120,8 @@ struct DState {
   int kbeg, kend, kb0, nblk;
   uint32_t koff;                 // per-lane K offset within a tile
   uint32_t voff[C::VLD];         // per-lane V offset of each 1-KB load (bf16: swizzled)
+  int cnew;                      // fused append: position of the new token (else -1)
+  const uint8_t *nk, *nv;        // fused append: its K and V rows (head g)
 };
 
 // Issue the K loads (into kr) and the V loads (into stage) of the block at
@@ -123,6 +131,35 @@ template <class C, int PS, bool FP8, int WAVES>
 __device__ __forceinline__ void issue_block(const DecodeArgs &a, const DState<C> &S, int kbase,
                                             KRegs<C> &kr, lds_u8 *stage) {
   const int lane = lane_id<WAVES>();
+  if constexpr (C::AP) {
+    if (S.cnew >= 0 && kbase + C::KB > S.cnew) {
+      // the block of the new token: its row comes from the input, the
+      // others (and clamped rows below it) from their page
+#pragma unroll
+      for (int tt = 0; tt < C::NT; ++tt) {
+        const int t0 = kbase + 16 * tt;
+        const int kp = min(t0, S.kend - 1);
+        const int pg = ldc(S.bt, __builtin_amdgcn_readfirstlane(kp / PS));
+        const size_t pbase = (size_t)pg * S.page_stride + S.head_off;
+        const int row0 = kp - kp % PS;
+        const int mk = min(t0 + (lane & 15), S.kend - 1);
+#pragma unroll
+        for (int i = 0; i < C::KLD; ++i) {
+          const uint32_t co = (uint32_t)(16 * (lane >> 4) + 64 * i);
+          kr.r[tt][i] = ld<u32x4>(mk == S.cnew ? S.nk + co : a.k + pbase + (size_t)(mk - row0) * C::RAW_ROW + co);
+        }
+        lds_u8 *vdst = stage + tt * 16 * C::RAW_ROW;
+#pragma unroll
+        for (int r = 0; r < C::VLD; ++r) {
+          const int rr = r * C::RPD + lane / C::RCH;
+          const int mv = min(t0 + rr, S.kend - 1);
+          const uint32_t co = (uint32_t)(16 * ((lane % C::RCH) ^ vswz<C::CH>(rr)));
+          dma16(mv == S.cnew ? S.nv + co : a.v + pbase + (size_t)(mv - row0) * C::RAW_ROW + co, vdst + r * 1024);
+        }
+      }
+      return;
+    }
+  }
   const bool whole = kbase + C::KB <= S.kend;
 #pragma unroll
   for (int tt = 0; tt < C::NT; ++tt) {
@@ -297,9 +334,10 @@ __device__ __forceinline__ void block_ready(const KRegs<C> &kr) {
 // One work item, run by one wave: partition `split` of the KV head and
 // head chunk `hy` (hy = head_chunks * g + chunk) of sequence `b`.  `lds`
 // holds DCfg::LDS bytes for this wave alone, 1024-aligned.
-template <int D, bool FP8, int PS, int WAVES = 1>
+// AP: fused append (DecodeArgs::k_new / v_new).
+template <int D, bool FP8, int PS, int WAVES = 1, bool AP = false>
 __device__ __forceinline__ void decode_item(const DecodeArgs &a, lds_u8 *lds, int split, int hy, int b) {
-  using C = DCfg<D, FP8, PS>;
+  using C = DCfg<D, FP8, PS, AP>;
   lds_u8 *const st0 = lds;
   lds_u8 *const st1 = st0 + C::VRAW;
   lds_u8 *const vwide = st0 + 2 * C::VRAW;  // fp8 only
@@ -335,6 +373,29 @@ __device__ __forceinline__ void decode_item(const DecodeArgs &a, lds_u8 *lds, in
     const int chunk = FP8 ? slot : slot ^ vswz<C::CH>(rr);
     S.voff[r] = (uint32_t)(rr * C::RAW_ROW + 16 * chunk);
   }
+  // Fused append: the new token (position c - 1) is read from the input by
+  // the partition that holds it, whose first head chunk also writes its K
+  // and V rows into the pool slot (lanes 0 .. 2 CH - 1, one 16-byte chunk
+  // each).  No work item reads that slot.
+  S.cnew = -1;
+  u32x4 apx{};
+  uint8_t *apdst = nullptr;
+  if constexpr (AP) {
+    S.nk = a.k_new + ((size_t)b * a.h_kv + g) * C::ROW;
+    S.nv = a.v_new + ((size_t)b * a.h_kv + g) * C::ROW;
+    if (split == nsplit - 1) {
+      S.cnew = c - 1;
+      if (hc == 0 && lane < 2 * C::CH) {
+        // V = K address plus the V - K distance (a per-lane choice between
+        // two pointers would index a copy of the arguments in scratch)
+        const int kv = lane / C::CH, cc = lane % C::CH;
+        apx = ld<u32x4>(S.nk + (kv ? S.nv - S.nk : 0) + 16 * cc);
+        const int pg = S.bt[(c - 1) / PS];
+        apdst = const_cast<uint8_t *>(a.k) + (kv ? a.v - a.k : 0) + (size_t)pg * S.page_stride + S.head_off +
+                (size_t)((c - 1) % PS) * C::RAW_ROW + 16 * cc;
+      }
+    }
+  }
 
   KRegs<C> k0, k1;
   issue_block<C, PS, FP8, WAVES>(a, S, S.kb0, k0, st0);
@@ -354,6 +415,9 @@ __device__ __forceinline__ void decode_item(const DecodeArgs &a, lds_u8 *lds, in
   for (int j = 0; j < S.nblk; j += 2) {
     const int kbase = S.kb0 + j * C::KB;
     block_ready<C>(k0);
+    if constexpr (AP) {
+      if (j == 0 && apdst) st<u32x4>(apdst, apx);
+    }
     if (j + 1 < S.nblk) issue_block<C, PS, FP8, WAVES>(a, S, kbase + C::KB, k1, st1);
     compute_block<C, PS, FP8, WAVES>(a, S, kbase, k0, st0, vwide, qf, o, m, l, g);
     if (j + 1 < S.nblk) {

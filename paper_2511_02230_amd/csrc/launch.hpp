@@ -42,12 +42,14 @@ hipError_t launch_decode_bf16(const PoolView &p, const BatchView &b, const void 
 // merges of split keys); results equal the two separate launches bit for bit
 // at the same decode partition length (mixed_split_len resolves 0).
 // interleave: groups of eight workgroups per run of one kind (0 = library
-// choice).
+// choice).  k_pf / v_pf and k_dc / v_dc (bf16 pools; null = already in the
+// pool): the new rows the launch appends itself.
 int mixed_split_len(const PoolView &p, const BatchView &db, int h_q, int requested);
 size_t mixed_workspace_bytes(const PoolView &p, const BatchView &pb, const BatchView &db, int h_q,
                              int split_len);
-hipError_t launch_mixed(const PoolView &p, const BatchView &pb, const void *q_pf, void *out_pf,
-                        const BatchView &db, const void *q_dc, void *out_dc, int h_q, float scale,
+hipError_t launch_mixed(const PoolView &p, const BatchView &pb, const void *q_pf, const void *k_pf,
+                        const void *v_pf, void *out_pf, const BatchView &db, const void *q_dc,
+                        const void *k_dc, const void *v_dc, void *out_dc, int h_q, float scale,
                         int window, int split_len, int interleave, void *ws, hipStream_t s);
 
 // Device address of the allocation-free decode's scratch on the current

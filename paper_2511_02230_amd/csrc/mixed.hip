@@ -50,7 +50,11 @@ __device__ __forceinline__ int dc_before(const MixedLayout &m, int i) {
   return (int)min(pat, (long long)m.dc_groups);
 }
 
-template <int D, int BN, bool FP8, int PS>
+// AP: fused append (bf16 pools): the prefill batch's new turn and the
+// decode batch's new tokens are written into the pool by this launch, and
+// read from the input rows by its work items (PrefillArgs / DecodeArgs
+// k_new, v_new; either pair may be null).
+template <int D, int BN, bool FP8, int PS, bool AP>
 __global__ __launch_bounds__(pf::kThreads, D >= 256 ? 1 : 2) void mixed_kernel(pf::PrefillArgs pa,
                                                                                dc::DecodeArgs da,
                                                                                MixedLayout m) {
@@ -70,24 +74,31 @@ __global__ __launch_bounds__(pf::kThreads, D >= 256 ? 1 : 2) void mixed_kernel(p
     if (d >= m.dc_items) return;
     const int split = d % m.dc_x;
     const int rest = d / m.dc_x;
-    dc::decode_item<D, FP8, PS, kWaves>(da, as_lds(lds_) + wave * DC::LDS, split, rest % m.dc_y,
-                                        rest / m.dc_y);
+    if (AP && da.k_new)
+      dc::decode_item<D, FP8, PS, kWaves, AP>(da, as_lds(lds_) + wave * DC::LDS, split, rest % m.dc_y,
+                                              rest / m.dc_y);
+    else
+      dc::decode_item<D, FP8, PS, kWaves>(da, as_lds(lds_) + wave * DC::LDS, split, rest % m.dc_y,
+                                          rest / m.dc_y);
   } else {
     const int p = (grp - before) * 8 + r;
     if (p >= m.pf_items) return;
     const int rest = p / m.pf_x;
-    pf::prefill_tile<D, BN, FP8, PS>(pa, as_lds(lds_), p % m.pf_x, rest % m.pf_y, rest / m.pf_y);
+    if (AP && pa.k_new)
+      pf::prefill_tile<D, BN, FP8, PS, AP>(pa, as_lds(lds_), p % m.pf_x, rest % m.pf_y, rest / m.pf_y);
+    else
+      pf::prefill_tile<D, BN, FP8, PS>(pa, as_lds(lds_), p % m.pf_x, rest % m.pf_y, rest / m.pf_y);
   }
 }
 
-template <int D, int BN, bool FP8>
+template <int D, int BN, bool FP8, bool AP = false>
 hipError_t launch(const pf::PrefillArgs &pa, const dc::DecodeArgs &da, const MixedLayout &m, int ps,
                   hipStream_t s) {
   const dim3 grid((unsigned)(8 * (m.pf_groups + m.dc_groups)));
   if (ps == 16)
-    hipLaunchKernelGGL((mixed_kernel<D, BN, FP8, 16>), grid, dim3(pf::kThreads), 0, s, pa, da, m);
+    hipLaunchKernelGGL((mixed_kernel<D, BN, FP8, 16, AP>), grid, dim3(pf::kThreads), 0, s, pa, da, m);
   else
-    hipLaunchKernelGGL((mixed_kernel<D, BN, FP8, 64>), grid, dim3(pf::kThreads), 0, s, pa, da, m);
+    hipLaunchKernelGGL((mixed_kernel<D, BN, FP8, 64, AP>), grid, dim3(pf::kThreads), 0, s, pa, da, m);
   return hipGetLastError();
 }
 
@@ -106,8 +117,9 @@ size_t mixed_workspace_bytes(const PoolView &p, const BatchView &pb, const Batch
   return (a + 255) / 256 * 256 + b;
 }
 
-hipError_t launch_mixed(const PoolView &p, const BatchView &pb, const void *q_pf, void *out_pf,
-                        const BatchView &db, const void *q_dc, void *out_dc, int h_q, float scale,
+hipError_t launch_mixed(const PoolView &p, const BatchView &pb, const void *q_pf, const void *k_pf,
+                        const void *v_pf, void *out_pf, const BatchView &db, const void *q_dc,
+                        const void *k_dc, const void *v_dc, void *out_dc, int h_q, float scale,
                         int window, int split_len, int interleave, void *ws, hipStream_t s) {
   const bool has_pf = pb.num_seqs > 0 && pb.max_q > 0 && pb.total_q > 0;
   const bool has_dc = db.num_seqs > 0;
@@ -119,6 +131,8 @@ hipError_t launch_mixed(const PoolView &p, const BatchView &pb, const void *q_pf
   if (has_pf) {
     const hipError_t e = prefill_args(p, pb, q_pf, h_q, scale, window, out_pf, w, pa);
     if (e != hipSuccess) return e;
+    pa.k_new = static_cast<const uint8_t *>(k_pf);
+    pa.v_new = static_cast<const uint8_t *>(v_pf);
     m.pf_x = p.h_kv * pa.splits;
     m.pf_y = pa.tiles;
     m.pf_items = m.pf_x * m.pf_y * pb.num_seqs;
@@ -126,6 +140,8 @@ hipError_t launch_mixed(const PoolView &p, const BatchView &pb, const void *q_pf
   if (has_dc) {
     decode_args(p, db, q_dc, h_q, scale, window, mixed_split_len(p, db, h_q, split_len), out_dc,
                 w + pf_ws, da);
+    da.k_new = static_cast<const uint8_t *>(k_dc);
+    da.v_new = static_cast<const uint8_t *>(v_dc);
     m.dc_x = da.max_splits | 1;  // the decode kernel's odd split stride
     m.dc_y = p.h_kv * da.head_chunks;
     m.dc_items = m.dc_x * m.dc_y * db.num_seqs;
@@ -152,16 +168,25 @@ hipError_t launch_mixed(const PoolView &p, const BatchView &pb, const void *q_pf
     m.half = dc_s < 0.05 * pf_s ? 0x3fffffff : 3 * (p.d >= 256 ? 1 : 2) * 256 / 8;
   }
   const bool fp8 = p.kv_dtype == 2;
+  const bool ap = (has_pf && k_pf) || (has_dc && k_dc);
+  if (ap && fp8) return hipErrorInvalidValue;  // rejected by the caller's checks
+  if (!has_pf) pa.k_new = pa.v_new = nullptr;
+  if (!has_dc) da.k_new = da.v_new = nullptr;
   hipError_t e = hipErrorInvalidValue;
   switch (p.d) {
     case 64:
-      e = fp8 ? launch<64, 64, true>(pa, da, m, p.ps, s) : launch<64, 64, false>(pa, da, m, p.ps, s);
+      e = fp8 ? launch<64, 64, true>(pa, da, m, p.ps, s)
+              : (ap ? launch<64, 64, false, true>(pa, da, m, p.ps, s) : launch<64, 64, false>(pa, da, m, p.ps, s));
       break;
     case 128:
-      e = fp8 ? launch<128, 64, true>(pa, da, m, p.ps, s) : launch<128, 64, false>(pa, da, m, p.ps, s);
+      e = fp8 ? launch<128, 64, true>(pa, da, m, p.ps, s)
+              : (ap ? launch<128, 64, false, true>(pa, da, m, p.ps, s)
+                    : launch<128, 64, false>(pa, da, m, p.ps, s));
       break;
     case 256:
-      e = fp8 ? launch<256, 32, true>(pa, da, m, p.ps, s) : launch<256, 64, false>(pa, da, m, p.ps, s);
+      e = fp8 ? launch<256, 32, true>(pa, da, m, p.ps, s)
+              : (ap ? launch<256, 64, false, true>(pa, da, m, p.ps, s)
+                    : launch<256, 64, false>(pa, da, m, p.ps, s));
       break;
   }
   if (e != hipSuccess) return e;

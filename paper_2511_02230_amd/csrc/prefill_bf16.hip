@@ -136,6 +136,7 @@ hipError_t prefill_args(const PoolView &p, const BatchView &b, const void *q, in
   a.bt = b.bt;
   a.ctx = b.ctx;
   a.cu = b.cu_q;
+  a.k_new = a.v_new = nullptr;  // no fused append
   a.num_seqs = b.num_seqs;
   a.max_pages = b.max_pages;
   a.h_q = h_q;

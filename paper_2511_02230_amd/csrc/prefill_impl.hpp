@@ -63,6 +63,10 @@ struct PrefillArgs {
   int32_t split_len;  // keys per partition (a multiple of the block size)
   float *part_o;      // splits > 1: [total_q * H_q][splits][D] fp32
   float *part_ml;     // splits > 1: [total_q * H_q][splits][2] (m, l)
+  // fused append (bf16 pools, Cfg::AP): the new turn's K and V rows
+  // [total_q][H_kv][D]; the kernel writes them into their pool slots and
+  // reads the new keys from here instead of from the pool
+  const uint8_t *k_new, *v_new;
 };
 
 constexpr int kRows = 128;  // rows per workgroup
@@ -79,8 +83,9 @@ __device__ __forceinline__ int pi_row(int m) {
   return 16 * (i >> 1) + 8 * h + 4 * (i & 1) + j;
 }
 
-template <int D, int BN, bool FP8, int PS>
+template <int D, int BN, bool FP8, int PS, bool APPEND = false>
 struct Cfg {
+  static constexpr bool AP = APPEND;                   // fused append (bf16 pools)
   static constexpr int ROW = D * 2;                    // bf16 bytes per key row in LDS
   static constexpr int CH = D / 8;                     // 16-byte chunks per bf16 row
   static constexpr int BN_ = BN;                       // keys per block
@@ -106,6 +111,7 @@ struct Cfg {
   static_assert(PS % RPD == 0, "a load never straddles a page");
   // two workgroups per CU below head_dim 256; one (as the registers allow) above
   static_assert(LDS <= (D >= 256 ? 160 : 80) * 1024, "LDS budget");
+  static_assert(!(AP && FP8), "the fused append writes bf16 rows");
 };
 
 // XOR swizzles of the 16-byte chunk index within a bf16 row.
@@ -183,10 +189,16 @@ __device__ __forceinline__ void block_pages(const int32_t *bt, int kbase, int kv
 // kv_end (last block only) are redirected to row kv_end - 1: valid, finite
 // data in the same page as the load's first row (or that row's page), which
 // the causal mask removes.
+//
+// With the fused append (C::AP), keys at or beyond `pnew` (the new turn) are
+// read from the caller's rows at `nsrc` (this wave's tensor, the sequence's
+// first new token, KV head g; consecutive tokens H_kv rows apart) through
+// per-lane addresses, on the blocks that hold any.
 template <class C, int PS, bool FP8, int LO = 0, int HI = C::DPW>
 __device__ __forceinline__ void issue_block(const PrefillArgs &a, const int32_t *bt, int g, int kbase,
                                             int kv_end, const int (&pg)[C::DPW],
-                                            const uint32_t (&loff)[C::DPW], lds_u8 *ring_stage) {
+                                            const uint32_t (&loff)[C::DPW], lds_u8 *ring_stage,
+                                            int pnew = 0, const uint8_t *nsrc = nullptr) {
   constexpr int HROWS = C::RAW_BLK / 2 / C::RAW_ROW;
   constexpr int NPW = HROWS > PS ? HROWS / PS : 1;
   constexpr int DPP = C::DPW / NPW;
@@ -196,6 +208,26 @@ __device__ __forceinline__ void issue_block(const PrefillArgs &a, const int32_t 
   const size_t page_stride = (size_t)a.h_kv * PS * C::RAW_ROW;
   const size_t head_off = (size_t)g * PS * C::RAW_ROW;
   lds_u8 *wdst = ring_stage + h * (C::RAW_BLK / 2);
+  if constexpr (C::AP) {
+    if (kbase + C::BN_ > pnew) {
+      // load i covers rows of page pg[i / DPP] (looked up by its first row,
+      // clamped); rows past kv_end repeat row kv_end - 1, a new-turn row, so
+      // every pool row read here lies in that page
+      const int lane = threadIdx.x & 63;
+      const size_t nstride = (size_t)a.h_kv * C::RAW_ROW;
+#pragma unroll
+      for (int i = LO; i < HI; ++i) {
+        const int r0 = kbase + h * HROWS + i * C::RPD;
+        const int kp = min(r0 + lane / C::RCH, kv_end - 1);
+        const uint32_t co = loff[i] % C::RAW_ROW;
+        const uint8_t *src =
+            kp >= pnew ? nsrc + (size_t)(kp - pnew) * nstride + co
+                       : tens + (size_t)pg[i / DPP] * page_stride + head_off + (size_t)(kp % PS) * C::RAW_ROW + co;
+        dma16(src, wdst + i * 1024);
+      }
+      return;
+    }
+  }
   if (kbase + C::BN_ <= kv_end) {
 #pragma unroll
     for (int p = 0; p < NPW; ++p) {
@@ -243,6 +275,8 @@ struct Tile {
   int kb_iss;              // first key of the block being issued (-1: none)
   lds_u8 *dst_iss;         // its ring stage
   int g, t, ipos, i_min, i_max, kv_end, kb_begin, nblk, half, col, gq, li;
+  int pnew;                // fused append: first new-turn position
+  const uint8_t *nsrc;     // fused append: this wave's tensor's new rows
   // per-lane LDS byte offsets within a bf16 block: V^T reads of output tile
   // dt (keys 8 (gq / 2) + li / 4, plus 32 tt + 16 ks and 4 for the second
   // read) and K reads of k-step ds (key pi(col), plus 32 tt).  The swizzles
@@ -427,7 +461,7 @@ __device__ __forceinline__ void issue_chunk(const PrefillArgs &a, const int32_t 
   if constexpr (K >= 1 && K < C::SPREAD) {
     if (T.kb_iss >= 0)
       issue_block<C, PS, FP8, K * C::DPW / C::SPREAD, (K + 1) * C::DPW / C::SPREAD>(
-          a, bt, T.g, T.kb_iss, T.kv_end, T.pg, T.loff, T.dst_iss);
+          a, bt, T.g, T.kb_iss, T.kv_end, T.pg, T.loff, T.dst_iss, T.pnew, T.nsrc);
   }
 }
 
@@ -576,9 +610,10 @@ __device__ __forceinline__ void wait_and_issue(const PrefillArgs &a, const int32
   }
   if (iss) {
     if constexpr (ALL || C::SPREAD == 1)
-      issue_block<C, PS, FP8>(a, bt, T.g, kb_iss, T.kv_end, T.pg, T.loff, dst);
+      issue_block<C, PS, FP8>(a, bt, T.g, kb_iss, T.kv_end, T.pg, T.loff, dst, T.pnew, T.nsrc);
     else
-      issue_block<C, PS, FP8, 0, C::DPW / C::SPREAD>(a, bt, T.g, kb_iss, T.kv_end, T.pg, T.loff, dst);
+      issue_block<C, PS, FP8, 0, C::DPW / C::SPREAD>(a, bt, T.g, kb_iss, T.kv_end, T.pg, T.loff, dst,
+                                                     T.pnew, T.nsrc);
   }
 }
 
@@ -597,13 +632,71 @@ __device__ __forceinline__ void step(const PrefillArgs &a, const int32_t *bt, Ti
   softmax_pv<C, PS, FP8>(a, bt, T, s_cur, ksc, vsc, vb, kb, s_nxt);
 }
 
+// Fused append: the new K and V rows that one workgroup writes into the
+// pool, in units of one 16-byte chunk: unit u is chunk u % CH of the K
+// ((u / CH) & 1 == 0) or V row of token tok_lo + u / (2 CH), KV head g.
+// Each thread moves up to NAP units per batch (all loads, then all stores),
+// held in vector values.  K and V addresses are the K address plus a
+// per-lane multiple of the V - K distance: a per-lane choice between two
+// pointer members would be compiled as a load from a dynamically indexed
+// copy of this struct in scratch memory.
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+template <class C, int PS>
+struct AppendRows {
+  static constexpr int NAP = C::CH >= 32 ? 2 : 4;  // head_dim 256: registers are scarce
+  const uint8_t *src_k;          // K row of token 0 of the sequence, head g
+  uint8_t *dst_k;                // K pool, head g of page 0
+  ptrdiff_t src_vk, dst_vk;      // V minus K addresses (input, pool)
+  const int32_t *bt;
+  int tok_lo, pos0, units, stride;  // stride: bytes between tokens in the input
+
+  __device__ __forceinline__ void load(int u0, u32x16 &x, u32x4 &pg) const {
+#pragma unroll
+    for (int k = 0; k < NAP; ++k) {
+      const int u = u0 + (int)threadIdx.x + k * kThreads;
+      if (u < units) {
+        const int tok = tok_lo + u / (2 * C::CH), kv = (u / C::CH) & 1, c = u % C::CH;
+        const u32x4 v = ld<u32x4>(src_k + (kv ? src_vk : 0) + (size_t)tok * stride + 16 * c);
+        x[4 * k] = v.x;
+        x[4 * k + 1] = v.y;
+        x[4 * k + 2] = v.z;
+        x[4 * k + 3] = v.w;
+        pg[k] = (uint32_t)bt[(pos0 + tok) / PS];
+      }
+    }
+  }
+  __device__ __forceinline__ void store(int u0, const u32x16 &x, const u32x4 &pg) const {
+    const size_t page_stride = (size_t)stride / C::ROW * PS * C::ROW;  // H_kv * PS rows
+#pragma unroll
+    for (int k = 0; k < NAP; ++k) {
+      const int u = u0 + (int)threadIdx.x + k * kThreads;
+      if (u < units) {
+        const int tok = tok_lo + u / (2 * C::CH), kv = (u / C::CH) & 1, c = u % C::CH;
+        const int pos = pos0 + tok;
+        st<u32x4>(dst_k + (kv ? dst_vk : 0) + (size_t)pg[k] * page_stride + (size_t)(pos % PS) * C::ROW + 16 * c,
+                  u32x4{x[4 * k], x[4 * k + 1], x[4 * k + 2], x[4 * k + 3]});
+      }
+    }
+  }
+  // units [u0, units), batch by batch
+  __device__ __forceinline__ void copy_from(int u0) const {
+    for (; u0 < units; u0 += NAP * kThreads) {
+      u32x16 x{};
+      u32x4 pg{};
+      load(u0, x, pg);
+      store(u0, x, pg);
+    }
+  }
+};
+
 // One work item: row tile `tile_rev` (counted from the last) of the
 // sequence of cost rank `rank`, KV head and key partition from `hx`
 // (hx = H_kv * split + g).  `lds` holds Cfg::LDS bytes, 1024-aligned.
-template <int D, int BN, bool FP8, int PS>
+// AP: fused append (PrefillArgs::k_new / v_new).
+template <int D, int BN, bool FP8, int PS, bool AP = false>
 __device__ __forceinline__ void prefill_tile(const PrefillArgs &a, lds_u8 *lds, int hx, int tile_rev,
                                              int rank) {
-  using C = Cfg<D, BN, FP8, PS>;
+  using C = Cfg<D, BN, FP8, PS, AP>;
   Rings<C> R;
   R.k = lds;
   R.v = R.k + 2 * C::RAW_BLK;
@@ -676,6 +769,30 @@ __device__ __forceinline__ void prefill_tile(const PrefillArgs &a, lds_u8 *lds, 
   T.kb_begin = max(kv_begin, part_lo) / BN;
   const int kb_end = (min(T.kv_end, part_hi) + BN - 1) / BN;
   T.nblk = kb_end - T.kb_begin;
+  // Fused append: keys from P on come from the input rows, and partition
+  // 0's workgroup writes the rows of the tokens whose first row t G lies in
+  // this tile (every token has exactly one such tile).  No workgroup reads
+  // the pool slots written here, so nothing orders the workgroups.
+  AppendRows<C, PS> ap;
+  T.pnew = 0;
+  T.nsrc = nullptr;
+  if constexpr (AP) {
+    T.pnew = P;
+    const size_t in_stride = (size_t)a.h_kv * C::ROW;
+    const size_t row0 = ((size_t)q0 * a.h_kv + g) * C::ROW;
+    ap.src_k = a.k_new + row0;
+    ap.src_vk = a.v_new - a.k_new;
+    T.nsrc = (T.t == 0 ? a.k_new : a.v_new) + row0;
+    ap.dst_k = const_cast<uint8_t *>(a.k) + (size_t)g * PS * C::ROW;
+    ap.dst_vk = a.v - a.k;
+    ap.bt = bt;
+    ap.pos0 = P;
+    ap.stride = (int)in_stride;
+    ap.tok_lo = __builtin_amdgcn_readfirstlane((R0 + G - 1) / G);
+    const int tok_hi = min(n, (R0 + kRows + G - 1) / G);
+    ap.units = split == 0 ? max(0, tok_hi - ap.tok_lo) * 2 * C::CH : 0;
+    if (T.nblk <= 0) ap.copy_from(0);
+  }
   const size_t prow = (size_t)(q0 + t) * a.h_q + (size_t)g * G + hh;  // (token, head) row
   if (T.nblk <= 0) {
     // an empty partition: weight 0 in the merge
@@ -691,8 +808,13 @@ __device__ __forceinline__ void prefill_tile(const PrefillArgs &a, lds_u8 *lds, 
   // block 0 is computed
   if (T.t == 0) {
     block_pages<C, PS>(bt, T.kb_begin * BN, T.kv_end, T.pg);
-    issue_block<C, PS, FP8>(a, bt, g, T.kb_begin * BN, T.kv_end, T.pg, T.loff, R.k);
+    issue_block<C, PS, FP8>(a, bt, g, T.kb_begin * BN, T.kv_end, T.pg, T.loff, R.k, T.pnew, T.nsrc);
   }
+  // fused append: the first batch of rows is loaded beside Q and stored
+  // once the prologue's loads have landed
+  u32x16 apx{};
+  u32x4 appg{};
+  if constexpr (AP) ap.load(0, apx, appg);
   // k-step s takes d = 16 s + 8 half + 0..7; fp8 pools pair the steps so
   // that one 16-code K read feeds two: d = 32 (s / 2) + 16 half + 8 (s % 2)
 #pragma unroll
@@ -709,6 +831,10 @@ __device__ __forceinline__ void prefill_tile(const PrefillArgs &a, lds_u8 *lds, 
 
   f32x16 sA[C::NT], sB[C::NT];
   wait_and_issue<C, PS, FP8, 1, true>(a, bt, T, -1, R);  // U = (-1) & 1
+  if constexpr (AP) {
+    ap.store(0, apx, appg);
+    ap.copy_from(AppendRows<C, PS>::NAP * kThreads);  // G < 4 (head_dim 128): more rows
+  }
   qk_part<C, 0>(R.k, T, sA);
   qk_part<C, 1>(R.k, T, sA);
 

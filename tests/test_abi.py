@@ -202,9 +202,9 @@ def test_mixed_launch_checks_arguments_on_the_host(ckv):
     E = _batch(ckv, num_seqs=0)
 
     def call(pb=PB, db=DB, qp=1, op=1, qd=1, od=1, qdt=1, hq=4, scale=0.1, w=0, split=0, inter=0,
-             ws=1, wsb=1 << 30):
-        return f(ctypes.byref(P), ctypes.byref(pb), qp, op, ctypes.byref(db), qd, od, qdt, hq, scale, w,
-                 split, inter, ws, wsb, None)
+             ws=1, wsb=1 << 30, kp=None, vp=None, kd=None, vd=None, pool=P):
+        return f(ctypes.byref(pool), ctypes.byref(pb), qp, kp, vp, op, ctypes.byref(db), qd, kd, vd, od, qdt,
+                 hq, scale, w, split, inter, ws, wsb, None)
 
     assert call(hq=3) == 1                 # 3 % 2
     assert call(qdt=0) == 2                # fp32 queries: no mixed kernel
@@ -220,3 +220,10 @@ def test_mixed_launch_checks_arguments_on_the_host(ckv):
     assert call(split=128, ws=None) == 3
     assert call(split=128, wsb=need - 1) == 3
     assert call(split=128, ws=1 << 20 | 16) == 1   # not 256-byte aligned
+    # fused append: rows come in K / V pairs, for bf16 pools only
+    assert call(kp=1) == 1
+    assert call(vd=1) == 1
+    F8 = _pool(ckv, num_pages=100000, kv_dtype=ckv.CKV_FP8_E4M3, k_scale=1, v_scale=1)
+    assert call(pool=F8, kp=1, vp=1) == 2
+    assert call(pool=F8, kd=1, vd=1) == 2
+    assert call(pool=F8, pb=E, db=E, kp=1, vp=1) == 0  # nothing to append

@@ -584,6 +584,114 @@ def test_mixed_launch_equals_the_separate_calls(case):
                 check_close(got[b], r, cfg, f"mixed decode seq {b} split {split}")
 
 
+def _empty_batch(ckv):
+    return ckv.Batch(torch.zeros((0, 1), dtype=torch.int32, device="cuda"),
+                     torch.zeros(0, dtype=torch.int32, device="cuda"),
+                     torch.zeros(1, dtype=torch.int32, device="cuda"), 0, 0, 0)
+
+
+def _pools_equal(a, b):
+    return (torch.equal(a.pool.k.view(torch.int16), b.pool.k.view(torch.int16))
+            and torch.equal(a.pool.v.view(torch.int16), b.pool.v.view(torch.int16)))
+
+
+MIXED_APPEND = [c for c in MIXED if c[0].kv_dtype == "bf16"] + [
+    # one query head per KV head: a tile owns 128 tokens, more rows than one
+    # batch of the workgroup's copy
+    (cfg_of("a1", 2, 2, 128, 16, "bf16"), [(100, 300), (0, 129)], [5, 1], 0),
+    (cfg_of("a2", 4, 2, 256, 64, "bf16"), [(70, 150), (0, 1)], [64, 65], 0),
+    # key partitions under a window: partition 0 of the late tiles is empty,
+    # and its workgroup still writes its tokens
+    (cfg_of("a3", 8, 1, 128, 16, "bf16"), [(6000, 64)], [6100, 100], 100),
+]
+
+
+@pytest.mark.parametrize("case", MIXED_APPEND, ids=lambda c: c[0].name)
+def test_mixed_launch_with_the_append_fused(case):
+    """Given the new K/V rows, mixed_attn leaves the whole pool exactly as
+    kv_append does (every other slot keeps its poison) and returns the bits
+    of the same launch over the appended pool, for the rows of both batches
+    at once or of one batch (the other appended beforehand), at several
+    interleavings; outputs within the bars of the oracle."""
+    from paper_2511_02230_amd import ckv
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    cfg, pf, dc, w = case
+    wl = workload.make_workload(cfg, prefill=pf, decode=dc)
+    say(f"case mixed+append {cfg.name} prefill={pf} decode={dc} W={w}")
+    H, D = cfg.num_q_heads, cfg.head_dim
+    has_p, has_d = wl.prefill.num_seqs > 0, wl.decode.num_seqs > 0
+    ref = DeviceWorkload(wl, "cuda", window=w)
+    if has_p:
+        ref.append_prefill()
+    if has_d:
+        ref.append_decode()
+    empty = _empty_batch(ckv)
+    qp = ref.q_prefill if has_p else torch.empty((0, H, D), dtype=torch.bfloat16, device="cuda")
+    qd = ref.q_decode if has_d else torch.empty((0, H, D), dtype=torch.bfloat16, device="cuda")
+    pbatch = ref.prefill if has_p else empty
+    dbatch = ref.decode if has_d else empty
+    rp, rd = ckv.mixed_attn(ref.pool, pbatch, qp, dbatch, qd, cfg.softmax_scale, w)
+    torch.cuda.synchronize()
+    for mode in ("both", "prefill", "decode"):
+        dw = DeviceWorkload(wl, "cuda", window=w)
+        fuse_p, fuse_d = has_p and mode != "decode", has_d and mode != "prefill"
+        if has_p and not fuse_p:
+            dw.append_prefill()
+        if has_d and not fuse_d:
+            dw.append_decode()
+        rows = dict(k_prefill=dw.k_new if fuse_p else None, v_prefill=dw.v_new if fuse_p else None,
+                    k_decode=dw.k_dec if fuse_d else None, v_decode=dw.v_dec if fuse_d else None)
+        for inter in (0, 1, 32):
+            op, od = ckv.mixed_attn(dw.pool, dw.prefill if has_p else empty, dw.q_prefill if has_p else qp,
+                                    dw.decode if has_d else empty, dw.q_decode if has_d else qd,
+                                    cfg.softmax_scale, w, 0, inter, **rows)
+            torch.cuda.synchronize()
+            assert _pools_equal(dw, ref), (mode, inter)
+            if has_p:
+                assert torch.equal(op.view(torch.int16), rp.view(torch.int16)), (mode, inter)
+            if has_d:
+                assert torch.equal(od.view(torch.int16), rd.view(torch.int16)), (mode, inter)
+        del dw
+    st = OracleState(wl, device="cuda")
+    if has_p:
+        st.append_prefill()
+        ref_o = st.prefill(to_numpy(ref.q_prefill), st.rows_of(wl.prefill), w)
+        got = out_f64(op)
+        cu = wl.prefill.cu_q_lens
+        for b, r in ref_o.items():
+            check_close(got[cu[b]:cu[b + 1]], r, cfg, f"fused-append prefill seq {b}")
+    if has_d:
+        st.append_decode()
+        ref_o = st.decode(to_numpy(ref.q_decode), st.rows_of(wl.decode), w)
+        got = out_f64(od)
+        for b, r in ref_o.items():
+            check_close(got[b], r, cfg, f"fused-append decode seq {b}")
+
+
+def test_mixed_launch_with_the_append_fused_full_config():
+    """The benchmark's whole Llama-3.1-70B step in one launch: the pool and
+    both outputs equal kv_append x2 followed by mixed_attn, bit for bit."""
+    from paper_2511_02230_amd import ckv
+    from paper_2511_02230_amd.harness import DeviceWorkload
+
+    cfg = workload.CONFIGS["llama3.1-70b"]
+    wl = workload.make_workload(cfg)
+    say("case mixed+append full llama3.1-70b")
+    ref = DeviceWorkload(wl, "cuda")
+    ref.append_prefill()
+    ref.append_decode()
+    rp, rd = ckv.mixed_attn(ref.pool, ref.prefill, ref.q_prefill, ref.decode, ref.q_decode, cfg.softmax_scale)
+    torch.cuda.synchronize()
+    dw = DeviceWorkload(wl, "cuda")
+    op, od = ckv.mixed_attn(dw.pool, dw.prefill, dw.q_prefill, dw.decode, dw.q_decode, cfg.softmax_scale,
+                            k_prefill=dw.k_new, v_prefill=dw.v_new, k_decode=dw.k_dec, v_decode=dw.v_dec)
+    torch.cuda.synchronize()
+    assert _pools_equal(dw, ref)
+    assert torch.equal(op.view(torch.int16), rp.view(torch.int16))
+    assert torch.equal(od.view(torch.int16), rd.view(torch.int16))
+
+
 @pytest.mark.parametrize("name", ["llama3.1-70b", "glm4.5-355b"])
 def test_mixed_launch_full_config(name):
     """The benchmark's mixed step at full size (decode partitions of 2048
