@@ -46,9 +46,78 @@ __device__ __forceinline__ u32x2 quantize8(u32x4 x, float s) {
   return out;
 }
 
+// Chunk u of a block's rows -> token (relative to t0), K (0) or V (1),
+// head and 16-byte chunk: u = ((t * 2 + kv) * h + hh) * units + c.  POW2:
+// units, h and ps are powers of two (shifts and masks instead of divisions).
+template <bool POW2>
+__device__ __forceinline__ void split_unit(const AppendArgs &a, int u, int &t, int &kv, int &hh, int &c) {
+  if constexpr (POW2) {
+    const int lu = a.lg_units, lh = a.lg_h;
+    c = u & (a.units - 1);
+    hh = (u >> lu) & (a.h - 1);
+    kv = (u >> (lu + lh)) & 1;
+    t = u >> (lu + lh + 1);
+  } else {
+    const int per_kv = a.h * a.units;
+    t = u / (2 * per_kv);
+    int r = u - t * 2 * per_kv;
+    kv = r / per_kv;
+    r -= kv * per_kv;
+    hh = r / a.units;
+    c = r - hh * a.units;
+  }
+}
+
 // Grid: x = token chunks of one sequence, y = sequence.  Each thread moves
 // 16-byte chunks; consecutive threads cover consecutive chunks of a row, and
 // a (token, head) row is contiguous both in the packed input and in its page.
+// A thread takes its chunks NB at a time: all loads (and page ids, then the
+// fp8 scales) first, then the stores, so the batch costs one round trip to
+// memory rather than one per chunk.  V addresses are K addresses plus the
+// V - K distance: a per-lane choice between the two pointer arguments would
+// be compiled as loads from the argument segment.
+template <bool FP8, bool POW2>
+__device__ __forceinline__ void append_block(const AppendArgs &a, int q0, int t0, int P, int total,
+                                             const int32_t *bt) {
+  constexpr int NB = 4;
+  const ptrdiff_t in_vk = a.v_new - a.k_new;
+  const ptrdiff_t pool_vk = a.v_pool - a.k_pool;
+  const ptrdiff_t sc_vk = FP8 ? a.v_scale - a.k_scale : 0;
+  for (int u0 = threadIdx.x; u0 < total; u0 += NB * blockDim.x) {
+    u32x4 x[NB];
+    int pg[NB], t[NB], kv[NB], hh[NB], c[NB];
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      const int u = u0 + k * blockDim.x;
+      if (u < total) {
+        split_unit<POW2>(a, u, t[k], kv[k], hh[k], c[k]);
+        t[k] += t0;
+        const int pos = P + t[k];
+        pg[k] = bt[POW2 ? pos >> a.lg_ps : pos / a.ps];
+        x[k] = ld<u32x4>(a.k_new + (kv[k] ? in_vk : 0) + ((size_t)(q0 + t[k]) * a.h + hh[k]) * a.in_row + c[k] * 16);
+      }
+    }
+    float sc[NB];
+    if constexpr (FP8) {
+#pragma unroll
+      for (int k = 0; k < NB; ++k)
+        if (u0 + k * (int)blockDim.x < total) sc[k] = (a.k_scale + (kv[k] ? sc_vk : 0))[(size_t)pg[k] * a.h + hh[k]];
+    }
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      if (u0 + k * (int)blockDim.x < total) {
+        const int pos = P + t[k];
+        const int slot = POW2 ? pos & (a.ps - 1) : pos - (pos / a.ps) * a.ps;
+        uint8_t *dst = a.k_pool + (kv[k] ? pool_vk : 0) + (((size_t)pg[k] * a.h + hh[k]) * a.ps + slot) * a.out_row;
+        if constexpr (!FP8)
+          st<u32x4>(dst + c[k] * 16, x[k]);
+        else
+          st<u32x2>(dst + c[k] * 8, quantize8(x[k], sc[k]));
+      }
+    }
+  }
+}
+
 template <bool FP8>
 __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
   const int b = blockIdx.y;
@@ -58,55 +127,12 @@ __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
   if (t0 >= n) return;
   const int P = a.ctx[b];
   const int tcount = min(a.tok_per_block, n - t0);
-  const int per_head = a.units;
-  const int per_kv = a.h * per_head;
-  const int per_tok = 2 * per_kv;
-  const int total = tcount * per_tok;
+  const int total = tcount * 2 * a.h * a.units;
   const int32_t *bt = a.bt + (size_t)b * a.max_pages;
-  if (a.lg_units >= 0) {
-    // power-of-two shapes: u = ((tt * 2 + kv) * h + hh) * units + c
-    const int lu = a.lg_units, lh = a.lg_h, lp = a.lg_ps;
-    for (int u = threadIdx.x; u < total; u += blockDim.x) {
-      const int c = u & (per_head - 1);
-      const int hh = (u >> lu) & (a.h - 1);
-      const int kv = (u >> (lu + lh)) & 1;
-      const int t = t0 + (u >> (lu + lh + 1));
-      const int pos = P + t;
-      const int page = bt[pos >> lp];
-      const int slot = pos & (a.ps - 1);
-      const uint8_t *src = (kv ? a.v_new : a.k_new) + ((size_t)(q0 + t) * a.h + hh) * a.in_row + c * 16;
-      uint8_t *dst = (kv ? a.v_pool : a.k_pool) + (((size_t)page * a.h + hh) * a.ps + slot) * a.out_row;
-      const u32x4 x = ld<u32x4>(src);
-      if constexpr (!FP8) {
-        st<u32x4>(dst + c * 16, x);
-      } else {
-        const float s = (kv ? a.v_scale : a.k_scale)[(size_t)page * a.h + hh];
-        st<u32x2>(dst + c * 8, quantize8(x, s));
-      }
-    }
-    return;
-  }
-  for (int u = threadIdx.x; u < total; u += blockDim.x) {
-    const int tt = u / per_tok;
-    int r = u - tt * per_tok;
-    const int kv = r / per_kv;
-    r -= kv * per_kv;
-    const int hh = r / per_head;
-    const int c = r - hh * per_head;
-    const int t = t0 + tt;
-    const int pos = P + t;
-    const int page = bt[pos / a.ps];
-    const int slot = pos - (pos / a.ps) * a.ps;
-    const uint8_t *src = (kv ? a.v_new : a.k_new) + ((size_t)(q0 + t) * a.h + hh) * a.in_row + c * 16;
-    uint8_t *dst = (kv ? a.v_pool : a.k_pool) + (((size_t)page * a.h + hh) * a.ps + slot) * a.out_row;
-    const u32x4 x = ld<u32x4>(src);
-    if constexpr (!FP8) {
-      st<u32x4>(dst + c * 16, x);
-    } else {
-      const float s = (kv ? a.v_scale : a.k_scale)[(size_t)page * a.h + hh];
-      st<u32x2>(dst + c * 8, quantize8(x, s));
-    }
-  }
+  if (a.lg_units >= 0)
+    append_block<FP8, true>(a, q0, t0, P, total, bt);
+  else
+    append_block<FP8, false>(a, q0, t0, P, total, bt);
 }
 
 }  // namespace
