@@ -636,7 +636,8 @@ __device__ __forceinline__ void step(const PrefillArgs &a, const int32_t *bt, Ti
 // pool, in units of one 16-byte chunk: unit u is chunk u % CH of the K
 // ((u / CH) & 1 == 0) or V row of token tok_lo + u / (2 CH), KV head g.
 // Each thread moves up to NAP units per batch (all loads, then all stores),
-// held in vector values.  K and V addresses are the K address plus a
+// held in vector values rather than arrays.  K and V addresses are the K
+// address plus a
 // per-lane multiple of the V - K distance: a per-lane choice between two
 // pointer members would be compiled as a load from a dynamically indexed
 // copy of this struct in scratch memory.
@@ -833,7 +834,8 @@ __device__ __forceinline__ void prefill_tile(const PrefillArgs &a, lds_u8 *lds, 
   wait_and_issue<C, PS, FP8, 1, true>(a, bt, T, -1, R);  // U = (-1) & 1
   if constexpr (AP) {
     ap.store(0, apx, appg);
-    ap.copy_from(AppendRows<C, PS>::NAP * kThreads);  // G < 4 (head_dim 128): more rows
+    // tiles that own more rows than one batch (few query heads per KV head)
+    ap.copy_from(AppendRows<C, PS>::NAP * kThreads);
   }
   qk_part<C, 0>(R.k, T, sA);
   qk_part<C, 1>(R.k, T, sA);
