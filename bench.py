@@ -77,7 +77,8 @@ def measured_traffic(kernel_key):
     """HBM bytes per launch that rocprofv3 measured for this kernel
     (FETCH_SIZE / WRITE_SIZE passes scaled by a plain copy's readings, kept in
     profiles/traffic.json), or None when there is no measurement or the
-    kernel's sources have changed since it was taken."""
+    code of the kernel's sources (comments aside) has changed since it was
+    taken."""
     import hashlib
 
     try:
@@ -89,11 +90,22 @@ def measured_traffic(kernel_key):
         return None
     h = hashlib.sha256()
     for src in entry["sources"]:
-        with open(os.path.join(ROOT, "paper_2511_02230_amd", "csrc", src), "rb") as f:
-            h.update(f.read())
-    if h.hexdigest()[:16] != entry["sources_sha256_16"]:
+        with open(os.path.join(ROOT, "paper_2511_02230_amd", "csrc", src)) as f:
+            h.update(code_text(f.read()).encode())
+    if h.hexdigest()[:16] != entry["code_sha256_16"]:
         return None
     return float(entry["bytes"])
+
+
+def code_text(src):
+    """A source file's code without its comments and with runs of whitespace
+    made one space: what the traffic entries' hashes cover, so that editing a
+    comment does not void a measurement while any change to the code does."""
+    import re
+
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return re.sub(r"\s+", " ", src).strip()
 
 
 def cpu_baseline(wl, window, budget_s=20.0):
