@@ -108,7 +108,7 @@ def code_text(src):
     return re.sub(r"\s+", " ", src).strip()
 
 
-def cpu_baseline(wl, window, budget_s=20.0):
+def cpu_baseline(wl, window, budget_s=30.0):
     """Time the fp64 oracle on a bounded sample of the same workload: new-turn
     rows of the longest prefill sequence (prefill TFLOP/s of the sample)."""
     from threadpoolctl import threadpool_info
