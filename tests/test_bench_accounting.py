@@ -59,3 +59,29 @@ def test_bench_refuses_more_than_one_gpu():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
                        text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_traffic_entry_follows_the_code_not_its_comments(tmp_path, monkeypatch):
+    """A stored HBM-traffic measurement stays valid when only comments or
+    spacing of its kernel's sources change, and is dropped when code does."""
+    import hashlib
+    import json
+    import shutil
+
+    src = "__global__ void k(int *p) {\n  p[0] = 1;  // one store\n}\n"
+    (tmp_path / "paper_2511_02230_amd" / "csrc").mkdir(parents=True)
+    (tmp_path / "profiles").mkdir()
+    kfile = tmp_path / "paper_2511_02230_amd" / "csrc" / "k.hip"
+    kfile.write_text(src)
+    h = hashlib.sha256(bench.code_text(src).encode()).hexdigest()[:16]
+    (tmp_path / "profiles" / "traffic.json").write_text(
+        json.dumps({"k": {"sources": ["k.hip"], "code_sha256_16": h, "bytes": 1234}}))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.measured_traffic("k") == 1234.0
+    kfile.write_text("/* a kernel */\n__global__ void k(int *p) {\n    p[0] = 1;   // a store\n}\n")
+    assert bench.measured_traffic("k") == 1234.0
+    kfile.write_text("__global__ void k(int *p) {\n  p[0] = 2;  // one store\n}\n")
+    assert bench.measured_traffic("k") is None
+    assert bench.measured_traffic("missing") is None
+    shutil.rmtree(tmp_path / "profiles")
+    assert bench.measured_traffic("k") is None
